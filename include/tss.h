@@ -1,0 +1,190 @@
+/*
+ * tss.h -- C ABI of the sparse-depth target verification step (TSS) on MI355X.
+ *
+ * The library verifies a chain or tree of drafted tokens with one forward pass
+ * of a LLaMA-shaped decoder in which the blocks named by a skip mask are
+ * bypassed, then takes the greedy accept decision.  Sources in the paper
+ * (arXiv 2609.26100, "TSS: Target-Side Sparsification for Speculative
+ * Decoding in Domain-Specific Large Language Models"):
+ *   - Method / Problem Formulation: the sparse verifier T_S is the target with
+ *     the blocks in S bypassed; S = {} is the dense verifier; the target
+ *     verifies the draft's candidate tokens in parallel.
+ *   - Method / Domain-Aware Skip Controller: the skip set is fixed for a whole
+ *     request (unknown domains fall back to the dense path), and before each
+ *     block the forward checks the layer index against it: a skipped block
+ *     passes its input hidden state through, with no attention and no
+ *     feed-forward work.
+ *   - Experiments / Models and speculative decoding methods, and Appendix /
+ *     Evaluation Protocol: greedy decoding (temperature 0) with the underlying
+ *     method's accept/reject logic unchanged.
+ *   - Appendix / Models: LLaMA targets (pre-norm RMSNorm blocks, rotary
+ *     embedding, multi-head attention, SwiGLU MLP, untied lm_head).
+ *
+ * Conventions shared by every call:
+ *   - Every function returning int returns TSS_OK (0) or a negative
+ *     tss_status; no C++ exception crosses the ABI.  A message for the last
+ *     failure of a context is available from tss_last_error().
+ *   - Layers are numbered from 0.  A skip mask is n_layers bytes, 1 = skip the
+ *     block, 0 = run it; a NULL mask means the sequence's mask (verify) and a
+ *     mask of all zeros is the dense verifier.
+ *   - The library never allocates device memory.  Packed weights, the
+ *     workspace and the KV pool are device buffers owned by the caller, who
+ *     keeps them alive for the context's lifetime.  Host arrays passed in are
+ *     only read during the call.
+ *   - All device work is enqueued on the HIP stream given to tss_create.
+ *     tss_verify and tss_prefill return after that work has finished.
+ *   - Validation finishes before any device work is enqueued and sequence
+ *     state changes only when a call succeeds.  A HIP error poisons the
+ *     context: every later call that touches the device returns TSS_ESTATE.
+ *   - A context is not thread-safe.
+ */
+#ifndef TSS_H
+#define TSS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tss_ctx tss_ctx;
+
+enum tss_status {
+  TSS_OK = 0,
+  TSS_EINVAL = -1,     /* bad argument: shape, pointer, token, tree, mask */
+  TSS_ENOSPACE = -2,   /* a caller buffer is smaller than the size query says */
+  TSS_ECAPACITY = -3,  /* the sequence's KV capacity would be exceeded */
+  TSS_ESTATE = -4,     /* wrong call order, stale KV for an active layer, or a poisoned context */
+  TSS_EHIP = -5        /* the HIP runtime reported an error (the context is poisoned) */
+};
+
+enum tss_dtype { TSS_F32 = 0, TSS_BF16 = 1 };
+
+/* tss_verify flags */
+enum tss_flags {
+  TSS_COMMIT = 1u      /* keep the K/V of the root and the accepted path; n_kv += accept_len + 1 */
+};
+
+/* Kernel kinds for tss_profile_kernel. */
+enum tss_kernel {
+  TSS_K_EMBED = 0,
+  TSS_K_QKV = 1,       /* RMSNorm + Q/K/V projection + rotary + KV append */
+  TSS_K_ATTN = 2,      /* tree-masked attention over the paged KV cache */
+  TSS_K_OPROJ = 3,     /* output projection + residual */
+  TSS_K_GATEUP = 4,    /* RMSNorm + gate/up projection + SwiGLU */
+  TSS_K_DOWN = 5,      /* down projection + residual */
+  TSS_K_LMHEAD = 6,    /* final RMSNorm + lm_head + per-tile argmax */
+  TSS_K_ACCEPT = 7,    /* argmax reduction + accept scan */
+  TSS_K_COMPACT = 8    /* moves the accepted tree path's K/V next to the context */
+};
+
+/* Model shape.  Constraints (checked by tss_cfg_check):
+ *   d_model == n_heads * head_dim; head_dim in {64, 128};
+ *   d_model and ffn_dim multiples of 32; vocab a multiple of 32;
+ *   1 <= max_nodes <= 64 (nodes of one verify, root included);
+ *   dtype TSS_BF16 (bf16 weights, KV and GEMM inputs; fp32 accumulation,
+ *   residual stream, softmax and logits) or TSS_F32 (everything fp32).
+ * The KV page size is fixed at 16 tokens. */
+typedef struct {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t ffn_dim;
+  int32_t vocab;
+  float rope_base;     /* rotary base, 10000 for LLaMA */
+  float rms_eps;       /* RMSNorm epsilon, 1e-6 */
+  int32_t dtype;       /* enum tss_dtype */
+  int32_t max_nodes;   /* most nodes one tss_verify / prefill chunk may carry */
+} tss_model_cfg;
+
+/* Checks the constraints above.  Pure host function.  TSS_OK or TSS_EINVAL. */
+int tss_cfg_check(const tss_model_cfg* cfg);
+
+/* Size queries (bytes); 0 when cfg is invalid. */
+size_t tss_weights_bytes(const tss_model_cfg* cfg);
+size_t tss_workspace_bytes(const tss_model_cfg* cfg);
+size_t tss_kv_bytes(const tss_model_cfg* cfg, int32_t n_seqs, int32_t max_tokens_per_seq);
+
+/* Creates a context bound to hip_stream (a hipStream_t; NULL = the null
+ * stream), a packed-weight buffer of tss_weights_bytes() and a workspace of
+ * tss_workspace_bytes(), both device memory owned by the caller. */
+int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, size_t weights_bytes,
+               void* dev_workspace, size_t workspace_bytes, tss_ctx** out);
+
+/* Loads host tensors first .. first+count-1 of the fixed tensor order into the
+ * packed device buffer (may be called several times, e.g. one tensor at a time
+ * to stream a large model).  Order, all row-major [out][in] in the cfg dtype
+ * (fp32, or bf16 bit patterns as uint16):
+ *   0: embed [vocab][d_model]
+ *   1 + 9*l + {0..8} for layer l: attn_norm [d], wq [d][d], wk [d][d],
+ *       wv [d][d], wo [d][d], mlp_norm [d], w_gate [ffn][d], w_up [ffn][d],
+ *       w_down [d][ffn]
+ *   1 + 9*n_layers: final_norm [d];   2 + 9*n_layers: lm_head [vocab][d]
+ * Returns when the copies are complete. */
+int tss_load_weights(tss_ctx* ctx, int32_t first, int32_t count, const void* const* host_tensors);
+
+/* Binds a KV pool of tss_kv_bytes(cfg, n_seqs, max_tokens_per_seq) bytes of
+ * device memory and resets every sequence to length 0.  page_order, if not
+ * NULL, lists a permutation of the pool's n_seqs * ceil(max_tokens/16) pages;
+ * sequence s owns the s-th run of pages in that order (NULL = identity). */
+int tss_kv_alloc(tss_ctx* ctx, int32_t n_seqs, int32_t max_tokens_per_seq, void* dev_pool, size_t pool_bytes,
+                 const int32_t* page_order);
+
+/* Sets the skip mask of a sequence (n_layers bytes of 0/1; NULL = dense).
+ * The mask is the sequence's default for prefill and verify. */
+int tss_set_skip_mask(tss_ctx* ctx, int32_t seq, const uint8_t* mask);
+
+/* Appends n context tokens to sequence seq under its skip mask: their K/V are
+ * computed and kept for every layer the mask runs. */
+int tss_prefill(tss_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n);
+
+/* One verification step.
+ *   draft_tokens[n_nodes]: node 0 is the root (the last committed token,
+ *     whose K/V are not cached yet); nodes 1.. are drafted tokens.
+ *   tree_parent[n_nodes]: parent[0] = -1 and 0 <= parent[i] < i; NULL = chain.
+ *   skip_mask: n_layers bytes or NULL for the sequence's mask.  Every layer the
+ *     mask runs must hold K/V for the whole committed context (TSS_ESTATE
+ *     otherwise).
+ * Node i sits at position n_kv + depth(i) and attends to the cached context and
+ * to itself and its ancestors.  Outputs: accept_len = depth of the deepest node
+ * whose root path matches the greedy (argmax, lowest index on ties) tokens,
+ * lowest node index among equal depths; next_token = the greedy token at that
+ * node (the bonus token).  With TSS_COMMIT the root and accepted path are kept
+ * for the layers that ran and n_kv grows by accept_len + 1. */
+int tss_verify(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent, int32_t n_nodes,
+               const uint8_t* skip_mask, uint32_t flags, int32_t* accept_len, int32_t* next_token);
+
+/* Copies the last verify's fp32 logits [n_nodes][vocab] / greedy tokens
+ * [n_nodes] to host memory.  n_nodes must not exceed the last verify's. */
+int tss_get_logits(tss_ctx* ctx, float* host_dst, int32_t n_nodes);
+int tss_get_greedy(tss_ctx* ctx, int32_t* host_dst, int32_t n_nodes);
+
+/* Committed length of a sequence, and rewinding it (n_kv <= current length). */
+int tss_seq_length(tss_ctx* ctx, int32_t seq, int32_t* n_kv);
+int tss_seq_truncate(tss_ctx* ctx, int32_t seq, int32_t n_kv);
+
+/* Pure host checks, the same code the calls above run. */
+int tss_validate_tree(const int32_t* parent, int32_t n_nodes, int32_t max_nodes);
+int tss_validate_mask(const uint8_t* mask, int32_t n_layers);
+/* depth[i] and anc[i] (bit j set iff node j is i or an ancestor of i). */
+int tss_tree_meta(const int32_t* parent, int32_t n_nodes, int32_t* depth, uint64_t* anc);
+
+/* Times one kernel launch per verify with HIP events on the context's stream:
+ * the launch of kind `kernel` (enum tss_kernel) for layer `layer` (ignored for
+ * kinds outside the layer loop).  kernel = -1 switches timing off.
+ * tss_profile_read returns the summed milliseconds and the launch count
+ * (reset != 0 clears them). */
+int tss_profile_kernel(tss_ctx* ctx, int32_t kernel, int32_t layer);
+int tss_profile_read(tss_ctx* ctx, double* total_ms, int64_t* count, int32_t reset);
+
+const char* tss_last_error(const tss_ctx* ctx);
+const char* tss_status_string(int status);
+void tss_destroy(tss_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TSS_H */

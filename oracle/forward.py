@@ -141,6 +141,11 @@ def _forward(model: OracleModel, seq: OracleSequence, tokens, parent, mask, with
     n_kv = seq.n_kv
     pos = n_kv + depth
     scale = dt.type(1.0 / np.sqrt(hd))
+    # node i sees every cached context row, itself and its ancestors
+    visible = np.zeros((M, n_kv + M), dtype=bool)
+    visible[:, :n_kv] = True
+    for i in range(M):
+        visible[i, [n_kv + j for j in vis[i]]] = True
 
     h = model.glob("embed")[tokens].astype(dt)                  # [M][d]
     new_kv = {}
@@ -157,16 +162,15 @@ def _forward(model: OracleModel, seq: OracleSequence, tokens, parent, mask, with
         q = rope(q, pos, s.rope_base)
         k = rope(k, pos, s.rope_base)
         new_kv[l] = (k, v)
-        o = np.zeros((M, H, hd), dtype=dt)
-        for i in range(M):
-            rows = sorted(vis[i])
-            Kc = np.concatenate([seq.K[l], k[rows]], axis=0)    # [n_kv + |vis|][H][hd]
-            Vc = np.concatenate([seq.V[l], v[rows]], axis=0)
-            for hh in range(H):
-                sc = (Kc[:, hh, :] @ q[i, hh, :]) * scale
-                p = np.exp(sc - sc.max())
-                p = p / p.sum()
-                o[i, hh, :] = p @ Vc[:, hh, :]
+        # masked attention: scores against every cached row and every node,
+        # with the keys node i may not see set to -inf before the softmax
+        Kall = np.concatenate([seq.K[l], k], axis=0)             # [n_kv + M][H][hd]
+        Vall = np.concatenate([seq.V[l], v], axis=0)
+        sc = np.matmul(q.transpose(1, 0, 2), Kall.transpose(1, 2, 0)) * scale   # [H][M][n_kv + M]
+        sc = np.where(visible[None, :, :], sc, -np.inf)
+        p = np.exp(sc - sc.max(axis=-1, keepdims=True))
+        p = p / p.sum(axis=-1, keepdims=True)
+        o = np.matmul(p, Vall.transpose(1, 0, 2)).transpose(1, 0, 2)           # [M][H][hd]
         h = h + o.reshape(M, H * hd) @ w["wo"].T
         x = rmsnorm(h, w["mlp_norm"], s.rms_eps)
         a = silu(x @ w["w_gate"].T) * (x @ w["w_up"].T)

@@ -1,0 +1,265 @@
+// Weight-streaming projection GEMM for the verify step on gfx950.
+//
+// y[m][n] = sum_k x[m][k] * W[n][k] for the few rows m of one verify step
+// (the root and its drafted nodes), i.e. the Q/K/V, O, gate/up, down and
+// lm_head projections of a LLaMA block (the block's attention and
+// feed-forward work that the skip rule removes for bypassed layers).
+//
+// At a handful of rows the product is bound by streaming W from HBM, so the
+// design is about bytes, not FLOPs:
+//   * W is pre-packed in 1 KiB MFMA-lane-ordered tiles (tss_internal.h): every
+//     wave-wide 16-byte load reads one contiguous KiB, and a workgroup streams
+//     one strip of 16 (or 32) output columns over the full K.
+//   * The waves of a workgroup split K; each wave keeps CPW chunk loads in
+//     flight, runs the MFMAs, and the partial sums meet in LDS in a fixed
+//     order (no atomics: results are bit-reproducible).
+//   * Rows are padded to 16 for the MFMA; padded rows load nothing.
+//   * bf16: W in bf16; the fp32 activations arrive as hi and lo bf16 planes
+//     and each W tile meets both (two v_mfma_f32_16x16x32_bf16), so the
+//     product keeps about 16 significant bits of the activation at no extra
+//     HBM traffic (MFMA is idle at these row counts).  f32: four
+//     v_mfma_f32_16x16x4_f32 per 16-byte chunk.
+// Epilogues fuse the element-wise work around each projection:
+//   EPI_QKV     RMSNorm row scale, rotate-half RoPE at each node's position,
+//               q to the workspace, k and v into the node's paged KV slot.
+//   EPI_RESID   residual add into h, then the next RMSNorm's input
+//               h * gain (activation planes) and per-strip sums of h^2.
+//   EPI_SWIGLU  RMSNorm row scale, silu(gate) * up.
+//   EPI_LOGITS  RMSNorm row scale, fp32 logits and per-strip argmax.
+#include "tss_internal.h"
+
+namespace tss {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <typename T>
+__device__ __forceinline__ f32x4 mfma_chunk(const uint4& a, const uint4& b, f32x4 c);
+
+template <>
+__device__ __forceinline__ f32x4 mfma_chunk<__bf16>(const uint4& a, const uint4& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                 0, 0, 0);
+}
+
+template <>
+__device__ __forceinline__ f32x4 mfma_chunk<float>(const uint4& a, const uint4& b, f32x4 c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+  return c;
+}
+
+__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+
+// Chunk loads in flight per wave (register budget of a 1024-thread
+// workgroup: 128 VGPRs per lane).
+template <int MT, int NT> struct Cpw {
+  static constexpr int v = (MT == 1 && NT == 1) ? 8 : ((MT * NT) <= 2 ? 4 : ((MT * NT) <= 4 ? 2 : 1));
+};
+
+template <typename T, int MT, int NT, int EPI>
+__global__ __launch_bounds__(1024) void k_gemm(GemmArgs a) {
+  constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
+  constexpr int KL = KC / 4;           // K elements per lane per tile
+  constexpr int CPW = Cpw<MT, NT>::v;
+  constexpr int S = Mode<T>::planes;
+  using KV = typename Mode<T>::KV;
+  constexpr int ROWS = MT * 16;
+  constexpr int COLS = NT * 16;
+  extern __shared__ float smem[];
+
+  const int waves = blockDim.x >> 6;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int strip = blockIdx.x;
+  const int M = a.M, K = a.K, nkc = a.nkc;
+  const uint8_t* wstrip = a.w + (size_t)strip * nkc * NT * kTileBytes + lane * 16;
+  const T* x = (const T*)a.x;
+
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int base = wave * CPW; base < nkc; base += waves * CPW) {
+    uint4 wv[CPW][NT];
+    uint4 xv[CPW][MT][S];
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int c = base + i;
+      const bool in = c < nkc;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        wv[i][nt] = in ? *(const uint4*)(wstrip + ((size_t)c * NT + nt) * kTileBytes) : uint4{0, 0, 0, 0};
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = mt * 16 + r16;
+        const size_t off = (size_t)m * K + (size_t)c * KC + grp * KL;
+#pragma unroll
+        for (int p = 0; p < S; ++p)
+          xv[i][mt][p] = (in && m < M) ? *(const uint4*)(x + p * a.x_plane + off) : uint4{0, 0, 0, 0};
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < CPW; ++i)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int p = 0; p < S; ++p) acc[mt][nt] = mfma_chunk<T>(xv[i][mt][p], wv[i][nt], acc[mt][nt]);
+  }
+
+  // LDS: red[waves][ROWS][COLS] | y[ROWS][COLS] | rscale[ROWS] | aux[ROWS][COLS]
+  float* red = smem;
+  float* yfin = red + waves * ROWS * COLS;
+  float* rscale = yfin + ROWS * COLS;
+  float* aux = rscale + ROWS;
+
+  // MFMA result layout: lane holds column r16, rows 4*grp + v.
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        red[(wave * ROWS + mt * 16 + grp * 4 + v) * COLS + nt * 16 + r16] = acc[mt][nt][v];
+
+  // RMSNorm row scale from the producer's partial sums (fixed order, so every
+  // workgroup derives the same value).
+  if (a.ss_in) {
+    for (int m = wave; m < M; m += waves) {
+      float s = 0.f;
+      for (int p = lane; p < a.ss_nparts; p += 64) s += a.ss_in[(size_t)p * a.Mp + m];
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+      if (lane == 0) rscale[m] = rsqrtf(s / (float)a.norm_dim + a.eps);
+    }
+  } else {
+    for (int m = threadIdx.x; m < M; m += blockDim.x) rscale[m] = 1.f;
+  }
+  __syncthreads();
+
+  for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
+    const int row = e / COLS, col = e % COLS;
+    float s = 0.f;
+    for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * COLS + col];
+    yfin[row * COLS + col] = s * rscale[row];
+  }
+  __syncthreads();
+
+  const int n0 = strip * COLS;
+  if constexpr (EPI == EPI_QKV) {
+    const int HD = a.head_dim, d = a.d;
+    const int d16 = d >> 4, hd16 = HD >> 4;
+    const int n_kv = a.sp->n_kv;
+    for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
+      const int row = e / COLS, col = e % COLS;
+      const int n = n0 + col;
+      const int tile = n >> 4, c = n & 15;
+      const int sec = tile / d16, ts = tile % d16;
+      const int head = ts / hd16, t = ts % hd16;
+      const int dim = c < 8 ? 8 * t + c : (HD >> 1) + 8 * t + (c - 8);
+      float val = yfin[row * COLS + col];
+      if (sec < 2) {
+        const float partner = yfin[row * COLS + (col ^ 8)];
+        const float2 cs = a.rope[(size_t)a.sp->pos[row] * (HD >> 1) + 8 * t + (c & 7)];
+        val = c < 8 ? val * cs.x - partner * cs.y : val * cs.x + partner * cs.y;
+      }
+      if (sec == 0) {
+        a.q[(size_t)row * d + head * HD + dim] = val;
+      } else {
+        const int slot = n_kv + row;
+        const int page = a.page_table[slot >> 4];
+        const int tin = slot & 15;
+        KV* blk = (KV*)a.kv_pages +
+                  ((((size_t)a.layer * a.n_pages_pool + page) * 2 + (sec - 1)) * a.n_heads + head) * (16 * (size_t)HD);
+        if (sec == 1)
+          blk[tin * HD + dim] = (KV)val;
+        else
+          blk[(tin >> 2) * HD * 4 + dim * 4 + (tin & 3)] = (KV)val;
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    const int N = a.N;
+    for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
+      const int row = e / COLS, col = e % COLS;
+      const size_t idx = (size_t)row * N + n0 + col;
+      const float hn = a.h[idx] + yfin[row * COLS + col];
+      a.h[idx] = hn;
+      store_act<T>(a.xn, a.xn_plane, idx, hn * a.g_next[n0 + col]);
+      aux[row * COLS + col] = hn * hn;
+    }
+    __syncthreads();
+    for (int row = threadIdx.x; row < M; row += blockDim.x) {
+      float s = 0.f;
+      for (int col = 0; col < COLS; ++col) s += aux[row * COLS + col];
+      a.ss_out[(size_t)strip * a.Mp + row] = s;
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    static_assert(NT == 2, "gate and up tiles pair up in one strip");
+    const int F = a.N >> 1;
+    for (int e = threadIdx.x; e < M * 16; e += blockDim.x) {
+      const int row = e >> 4, c = e & 15;
+      const float g = yfin[row * COLS + c];
+      const float u = yfin[row * COLS + 16 + c];
+      store_act<T>(a.act, a.act_plane, (size_t)row * F + strip * 16 + c, silu(g) * u);
+    }
+  } else {  // EPI_LOGITS
+    const int N = a.N;
+    for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
+      const int row = e / COLS, col = e % COLS;
+      a.logits[(size_t)row * N + n0 + col] = yfin[row * COLS + col];
+    }
+    for (int row = threadIdx.x; row < M; row += blockDim.x) {
+      float bv = yfin[row * COLS];
+      int bi = 0;
+      for (int col = 1; col < COLS; ++col) {
+        const float v = yfin[row * COLS + col];
+        if (v > bv) { bv = v; bi = col; }
+      }
+      a.am_val[(size_t)strip * a.Mp + row] = bv;
+      a.am_idx[(size_t)strip * a.Mp + row] = n0 + bi;
+    }
+  }
+}
+
+template <typename T, int MT>
+static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
+  const int nt = strip_tiles(epi);
+  const int strips = a.N / (16 * nt);
+  const int cpw = nt == 2 ? Cpw<MT, 2>::v : Cpw<MT, 1>::v;
+  // enough waves to cover K with CPW-chunk blocks, capped by LDS (64 KiB) and 16
+  int waves = (a.nkc + cpw - 1) / cpw;
+  if (waves > 16) waves = 16;
+  const int rows = MT * 16, cols = nt * 16;
+  while (waves > 1 && (size_t)(waves * rows * cols + rows * cols * 2 + rows) * 4 > 65536) waves >>= 1;
+  const size_t lds = (size_t)(waves * rows * cols + rows * cols * 2 + rows) * 4;
+  dim3 grid(strips), block(waves * 64);
+  switch (epi) {
+    case EPI_QKV: hipLaunchKernelGGL((k_gemm<T, MT, 1, EPI_QKV>), grid, block, lds, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((k_gemm<T, MT, 1, EPI_RESID>), grid, block, lds, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((k_gemm<T, MT, 2, EPI_SWIGLU>), grid, block, lds, s, a); break;
+    default: hipLaunchKernelGGL((k_gemm<T, MT, 1, EPI_LOGITS>), grid, block, lds, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_t(int epi, int mt, const GemmArgs& a, hipStream_t s) {
+  switch (mt) {
+    case 1: return launch_mt<T, 1>(epi, a, s);
+    case 2: return launch_mt<T, 2>(epi, a, s);
+    case 3: return launch_mt<T, 3>(epi, a, s);
+    default: return launch_mt<T, 4>(epi, a, s);
+  }
+}
+
+hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_t s) {
+  return bf16 ? launch_t<__bf16>(epi, mt, a, s) : launch_t<float>(epi, mt, a, s);
+}
+
+}  // namespace tss

@@ -1,0 +1,848 @@
+// Host runtime of the sparse-depth verification step: the C ABI of tss.h.
+//
+// It owns no device memory.  It validates inputs, packs weights into the
+// caller's buffer, keeps per-sequence KV bookkeeping (committed length and,
+// per layer, how many committed rows hold K/V), derives tree metadata, and
+// enqueues the kernels on the caller's stream.  The skip rule of the paper's
+// Domain-Aware Skip Controller (before block l, check l against the skip set;
+// a skipped block passes the hidden state through) is applied here: the layer
+// loop launches nothing for a skipped block, so its weights and KV pages are
+// never read or written.
+#include "../../include/tss.h"
+#include "tss_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <thread>
+#include <vector>
+
+using namespace tss;
+
+namespace {
+
+constexpr int kMaxSplit = 64;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct LayerW {
+  size_t attn_norm, qkv, o, mlp_norm, gateup, down;
+};
+
+struct WeightLayout {
+  size_t embed = 0, final_norm = 0, lm_head = 0, total = 0;
+  std::vector<LayerW> layers;
+};
+
+struct WsLayout {
+  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, logits, am_val, am_idx, greedy, total;
+};
+
+// weight element bytes; the KV cache uses the same width (fp16 in the bf16
+// mode, fp32 in the f32 mode)
+int elem_size(const tss_model_cfg* c) { return c->dtype == TSS_BF16 ? 2 : 4; }
+// activation planes: two bf16 planes (hi, lo) in the bf16 mode, one fp32 plane otherwise
+int act_planes(const tss_model_cfg* c) { return c->dtype == TSS_BF16 ? 2 : 1; }
+int round16(int x) { return (x + 15) & ~15; }
+
+int cfg_ok(const tss_model_cfg* c) {
+  if (!c) return 0;
+  if (c->n_layers < 1 || c->n_layers > kMaxLayers) return 0;
+  if (c->head_dim != 64 && c->head_dim != 128) return 0;
+  if (c->n_heads < 1 || c->d_model != c->n_heads * c->head_dim) return 0;
+  if (c->d_model % 32 || c->ffn_dim < 32 || c->ffn_dim % 32 || c->vocab < 32 || c->vocab % 32) return 0;
+  if (c->dtype != TSS_F32 && c->dtype != TSS_BF16) return 0;
+  if (c->max_nodes < 1 || c->max_nodes > kMaxNodes) return 0;
+  if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return 0;
+  return 1;
+}
+
+WeightLayout weight_layout(const tss_model_cfg* c) {
+  WeightLayout w;
+  const size_t es = elem_size(c), d = c->d_model, f = c->ffn_dim, v = c->vocab;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return o; };
+  w.embed = take(v * d * es);
+  w.layers.resize(c->n_layers);
+  for (auto& L : w.layers) {
+    L.attn_norm = take(d * 4);
+    L.qkv = take(3 * d * d * es);
+    L.o = take(d * d * es);
+    L.mlp_norm = take(d * 4);
+    L.gateup = take(2 * f * d * es);
+    L.down = take(d * f * es);
+  }
+  w.final_norm = take(d * 4);
+  w.lm_head = take(v * d * es);
+  w.total = off;
+  return w;
+}
+
+WsLayout ws_layout(const tss_model_cfg* c) {
+  WsLayout w;
+  const size_t es = elem_size(c), d = c->d_model, f = c->ffn_dim, v = c->vocab;
+  const size_t Mp = round16(c->max_nodes);
+  const size_t ap = act_planes(c);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return o; };
+  w.sp = take(sizeof(StepParams));
+  w.result = take(sizeof(Result));
+  w.h = take(Mp * d * 4);
+  w.xa = take(ap * Mp * d * es);
+  w.xm = take(ap * Mp * d * es);
+  w.ss_a = take((d / 16) * Mp * 4);
+  w.ss_m = take((d / 16) * Mp * 4);
+  w.q = take(Mp * d * 4);
+  w.o = take(ap * Mp * d * es);
+  w.act = take(ap * Mp * f * es);
+  w.part_o = take((size_t)c->n_heads * kMaxSplit * Mp * c->head_dim * 4);
+  w.part_ml = take((size_t)c->n_heads * kMaxSplit * Mp * 2 * 4);
+  w.logits = take(Mp * v * 4);
+  w.am_val = take((v / 16) * Mp * 4);
+  w.am_idx = take((v / 16) * Mp * 4);
+  w.greedy = take(Mp * 4);
+  w.total = off;
+  return w;
+}
+
+struct KvLayout {
+  int pages_per_seq = 0, n_pages = 0;
+  size_t page_table = 0, rope = 0, pages = 0, total = 0;
+};
+
+KvLayout kv_layout(const tss_model_cfg* c, int n_seqs, int max_tokens) {
+  KvLayout k;
+  k.pages_per_seq = (max_tokens + kPage - 1) / kPage;
+  k.n_pages = n_seqs * k.pages_per_seq;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return o; };
+  k.page_table = take((size_t)k.n_pages * 4);
+  k.rope = take((size_t)max_tokens * (c->head_dim / 2) * sizeof(float2));
+  k.pages = take((size_t)c->n_layers * k.n_pages * 2 * c->n_heads * kPage * c->head_dim * elem_size(c));
+  k.total = off;
+  return k;
+}
+
+}  // namespace
+
+struct tss_ctx {
+  tss_model_cfg cfg{};
+  bool bf16 = false;
+  int es = 4, Mp = 16, KC = 16;
+  hipStream_t stream = nullptr;
+  uint8_t* w = nullptr;
+  uint8_t* ws = nullptr;
+  WeightLayout wl;
+  WsLayout wsl{};
+  // KV pool
+  uint8_t* kv = nullptr;
+  KvLayout kvl;
+  int n_seqs = 0, max_tokens = 0;
+  std::vector<int32_t> n_kv;
+  std::vector<std::vector<int32_t>> kv_len;
+  std::vector<std::vector<uint8_t>> mask;
+  // pinned host staging
+  StepParams* sp_host = nullptr;
+  Result* res_host = nullptr;
+  int last_M = 0;
+  bool poisoned = false;
+  std::string err;
+  // one-launch event timing
+  int prof_kind = -1, prof_layer = -1;
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  bool prof_armed = false;
+  double prof_ms = 0.0;
+  int64_t prof_count = 0;
+};
+
+namespace {
+
+int fail(tss_ctx* c, int code, const std::string& msg) {
+  if (c) c->err = msg;
+  return code;
+}
+
+int hip_fail(tss_ctx* c, hipError_t e, const char* where) {
+  c->poisoned = true;
+  return fail(c, TSS_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+#define HIPCHK(call, where)                      \
+  do {                                           \
+    hipError_t e_ = (call);                      \
+    if (e_ != hipSuccess) return hip_fail(c, e_, where); \
+  } while (0)
+
+int validate_tree(const int32_t* parent, int32_t n, int32_t max_nodes) {
+  if (n < 1 || n > max_nodes || n > kMaxNodes) return TSS_EINVAL;
+  if (!parent) return TSS_OK;
+  if (parent[0] != -1) return TSS_EINVAL;
+  for (int i = 1; i < n; ++i)
+    if (parent[i] < 0 || parent[i] >= i) return TSS_EINVAL;
+  return TSS_OK;
+}
+
+void tree_meta(const int32_t* parent, int n, int32_t* depth, uint64_t* anc) {
+  depth[0] = 0;
+  anc[0] = 1ull;
+  for (int i = 1; i < n; ++i) {
+    const int p = parent ? parent[i] : i - 1;
+    depth[i] = depth[p] + 1;
+    anc[i] = anc[p] | (1ull << i);
+  }
+}
+
+// Row permutation of the packed Q/K/V sections: inside each head, tile t of 16
+// output rows holds dims 8t..8t+7 and hd/2+8t..hd/2+8t+7, so every rotary pair
+// (j, j + hd/2) lands in one tile, 8 lanes apart.
+int qkv_src_row(int n_in_section, int head_dim) {
+  const int ts = n_in_section >> 4, c = n_in_section & 15;
+  const int hd16 = head_dim >> 4;
+  const int head = ts / hd16, t = ts % hd16;
+  const int dim = c < 8 ? 8 * t + c : head_dim / 2 + 8 * t + (c - 8);
+  return head * head_dim + dim;
+}
+
+// Packs rows of src [rows][K] (elements of es bytes) into 1 KiB lane-ordered
+// tiles.  Output tile (r, c) for row tile r and K chunk c is written to
+// dst + (r * nkc + c) * tile_stride; row_map gives the source row of packed row n.
+template <typename RowMap>
+void pack_tiles(uint8_t* dst, const uint8_t* src, int rows, int K, int es, size_t tile_stride, RowMap row_map) {
+  const int KC = 64 / es, KL = KC / 4;
+  const int nkc = K / KC;
+  const int row_tiles = rows / 16;
+  const unsigned nth = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+  auto work = [&](int r0, int r1) {
+    for (int r = r0; r < r1; ++r) {
+      const uint8_t* srow[16];
+      for (int i = 0; i < 16; ++i) srow[i] = src + (size_t)row_map(r * 16 + i) * K * es;
+      for (int c = 0; c < nkc; ++c) {
+        uint8_t* t = dst + ((size_t)r * nkc + c) * tile_stride;
+        for (int l = 0; l < 64; ++l)
+          std::memcpy(t + l * 16, srow[l & 15] + ((size_t)c * KC + (l >> 4) * KL) * es, 16);
+      }
+    }
+  };
+  if (row_tiles < 64 || nth == 1) {
+    work(0, row_tiles);
+    return;
+  }
+  std::vector<std::thread> th;
+  const int per = (row_tiles + nth - 1) / nth;
+  for (unsigned i = 0; i < nth; ++i) {
+    const int r0 = i * per, r1 = std::min(row_tiles, (int)(r0 + per));
+    if (r0 < r1) th.emplace_back(work, r0, r1);
+  }
+  for (auto& t : th) t.join();
+}
+
+bool mask_ok(const uint8_t* m, int n) {
+  for (int i = 0; i < n; ++i)
+    if (m[i] > 1) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tss_cfg_check(const tss_model_cfg* cfg) { return cfg_ok(cfg) ? TSS_OK : TSS_EINVAL; }
+
+size_t tss_weights_bytes(const tss_model_cfg* cfg) { return cfg_ok(cfg) ? weight_layout(cfg).total : 0; }
+
+size_t tss_workspace_bytes(const tss_model_cfg* cfg) { return cfg_ok(cfg) ? ws_layout(cfg).total : 0; }
+
+size_t tss_kv_bytes(const tss_model_cfg* cfg, int32_t n_seqs, int32_t max_tokens_per_seq) {
+  if (!cfg_ok(cfg) || n_seqs < 1 || max_tokens_per_seq < 1) return 0;
+  return kv_layout(cfg, n_seqs, max_tokens_per_seq).total;
+}
+
+int tss_validate_tree(const int32_t* parent, int32_t n_nodes, int32_t max_nodes) {
+  return validate_tree(parent, n_nodes, max_nodes);
+}
+
+int tss_validate_mask(const uint8_t* mask, int32_t n_layers) {
+  if (n_layers < 1 || n_layers > kMaxLayers) return TSS_EINVAL;
+  if (!mask) return TSS_OK;
+  return mask_ok(mask, n_layers) ? TSS_OK : TSS_EINVAL;
+}
+
+int tss_tree_meta(const int32_t* parent, int32_t n_nodes, int32_t* depth, uint64_t* anc) {
+  if (!depth || !anc) return TSS_EINVAL;
+  const int r = validate_tree(parent, n_nodes, kMaxNodes);
+  if (r != TSS_OK) return r;
+  tree_meta(parent, n_nodes, depth, anc);
+  return TSS_OK;
+}
+
+const char* tss_status_string(int s) {
+  switch (s) {
+    case TSS_OK: return "ok";
+    case TSS_EINVAL: return "invalid argument";
+    case TSS_ENOSPACE: return "buffer too small";
+    case TSS_ECAPACITY: return "KV capacity exceeded";
+    case TSS_ESTATE: return "invalid state";
+    case TSS_EHIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* tss_last_error(const tss_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, size_t weights_bytes,
+               void* dev_workspace, size_t workspace_bytes, tss_ctx** out) {
+  if (!out) return TSS_EINVAL;
+  *out = nullptr;
+  if (!cfg_ok(cfg) || !dev_weights || !dev_workspace) return TSS_EINVAL;
+  if (weights_bytes < weight_layout(cfg).total || workspace_bytes < ws_layout(cfg).total) return TSS_ENOSPACE;
+  tss_ctx* c = new tss_ctx();
+  c->cfg = *cfg;
+  c->bf16 = cfg->dtype == TSS_BF16;
+  c->es = elem_size(cfg);
+  c->KC = 64 / c->es;
+  c->Mp = round16(cfg->max_nodes);
+  c->stream = (hipStream_t)hip_stream;
+  c->w = (uint8_t*)dev_weights;
+  c->ws = (uint8_t*)dev_workspace;
+  c->wl = weight_layout(cfg);
+  c->wsl = ws_layout(cfg);
+  hipError_t e = hipHostMalloc((void**)&c->sp_host, sizeof(StepParams), hipHostMallocDefault);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&c->res_host, sizeof(Result), hipHostMallocDefault);
+  if (e == hipSuccess) e = hipEventCreate(&c->ev0);
+  if (e == hipSuccess) e = hipEventCreate(&c->ev1);
+  if (e != hipSuccess) {
+    tss_destroy(c);
+    return TSS_EHIP;
+  }
+  *out = c;
+  return TSS_OK;
+}
+
+void tss_destroy(tss_ctx* c) {
+  if (!c) return;
+  if (c->sp_host) (void)hipHostFree(c->sp_host);
+  if (c->res_host) (void)hipHostFree(c->res_host);
+  if (c->ev0) (void)hipEventDestroy(c->ev0);
+  if (c->ev1) (void)hipEventDestroy(c->ev1);
+  delete c;
+}
+
+int tss_load_weights(tss_ctx* c, int32_t first, int32_t count, const void* const* host_tensors) {
+  if (!c) return TSS_EINVAL;
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  const int L = c->cfg.n_layers, d = c->cfg.d_model, f = c->cfg.ffn_dim, v = c->cfg.vocab, es = c->es;
+  const int total = 3 + 9 * L;
+  if (!host_tensors || first < 0 || count < 1 || first + count > total)
+    return fail(c, TSS_EINVAL, "tensor range outside the model's tensor list");
+  for (int i = 0; i < count; ++i)
+    if (!host_tensors[i]) return fail(c, TSS_EINVAL, "null tensor pointer");
+  HIPCHK(hipStreamSynchronize(c->stream), "sync before weight load");
+  std::vector<uint8_t> buf;
+  auto h2d = [&](size_t off, const void* src, size_t bytes) {
+    return hipMemcpy(c->w + off, src, bytes, hipMemcpyHostToDevice);
+  };
+  auto gain = [&](size_t off, const void* src) {
+    std::vector<float> g(d);
+    if (c->bf16) {
+      const uint16_t* s = (const uint16_t*)src;
+      for (int k = 0; k < d; ++k) {
+        const uint32_t b = (uint32_t)s[k] << 16;
+        std::memcpy(&g[k], &b, 4);
+      }
+    } else {
+      std::memcpy(g.data(), src, (size_t)d * 4);
+    }
+    return h2d(off, g.data(), (size_t)d * 4);
+  };
+  auto plain = [&](size_t off, const void* src, int rows, int K) {
+    buf.resize((size_t)rows * K * es);
+    pack_tiles(buf.data(), (const uint8_t*)src, rows, K, es, kTileBytes, [](int n) { return n; });
+    return h2d(off, buf.data(), buf.size());
+  };
+  for (int i = 0; i < count; ++i) {
+    const int t = first + i;
+    const void* src = host_tensors[i];
+    hipError_t e = hipSuccess;
+    if (t == 0) {
+      e = h2d(c->wl.embed, src, (size_t)v * d * es);
+    } else if (t == 1 + 9 * L) {
+      e = gain(c->wl.final_norm, src);
+    } else if (t == 2 + 9 * L) {
+      e = plain(c->wl.lm_head, src, v, d);
+    } else {
+      const int l = (t - 1) / 9, j = (t - 1) % 9;
+      const LayerW& W = c->wl.layers[l];
+      switch (j) {
+        case 0: e = gain(W.attn_norm, src); break;
+        case 1: case 2: case 3: {
+          const int hd = c->cfg.head_dim;
+          buf.resize((size_t)d * d * es);
+          pack_tiles(buf.data(), (const uint8_t*)src, d, d, es, kTileBytes,
+                     [hd](int n) { return qkv_src_row(n, hd); });
+          e = h2d(W.qkv + (size_t)(j - 1) * d * d * es, buf.data(), buf.size());
+          break;
+        }
+        case 4: e = plain(W.o, src, d, d); break;
+        case 5: e = gain(W.mlp_norm, src); break;
+        case 6: case 7: {
+          // gate tile s and up tile s share strip s: 2 KiB per K chunk, gate first
+          buf.resize((size_t)f * d * es);
+          pack_tiles(buf.data(), (const uint8_t*)src, f, d, es, kTileBytes, [](int n) { return n; });
+          const size_t n_tiles = (size_t)(f / 16) * (d / c->KC);
+          e = hipMemcpy2D(c->w + W.gateup + (j - 6) * kTileBytes, 2 * kTileBytes, buf.data(), kTileBytes, kTileBytes,
+                          n_tiles, hipMemcpyHostToDevice);
+          break;
+        }
+        default: e = plain(W.down, src, d, f); break;
+      }
+    }
+    if (e != hipSuccess) return hip_fail(c, e, "weight upload");
+  }
+  return TSS_OK;
+}
+
+int tss_kv_alloc(tss_ctx* c, int32_t n_seqs, int32_t max_tokens_per_seq, void* dev_pool, size_t pool_bytes,
+                 const int32_t* page_order) {
+  if (!c) return TSS_EINVAL;
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  if (n_seqs < 1 || max_tokens_per_seq < 1 || !dev_pool) return fail(c, TSS_EINVAL, "bad KV pool arguments");
+  const KvLayout k = kv_layout(&c->cfg, n_seqs, max_tokens_per_seq);
+  if (pool_bytes < k.total) return fail(c, TSS_ENOSPACE, "KV pool smaller than tss_kv_bytes()");
+  std::vector<int32_t> pt(k.n_pages);
+  if (page_order) {
+    std::vector<uint8_t> seen(k.n_pages, 0);
+    for (int i = 0; i < k.n_pages; ++i) {
+      const int p = page_order[i];
+      if (p < 0 || p >= k.n_pages || seen[p]) return fail(c, TSS_EINVAL, "page_order is not a permutation");
+      seen[p] = 1;
+      pt[i] = p;
+    }
+  } else {
+    for (int i = 0; i < k.n_pages; ++i) pt[i] = i;
+  }
+  HIPCHK(hipStreamSynchronize(c->stream), "sync before KV bind");
+  c->kv = (uint8_t*)dev_pool;
+  c->kvl = k;
+  c->n_seqs = n_seqs;
+  c->max_tokens = max_tokens_per_seq;
+  HIPCHK(hipMemcpy(c->kv + k.page_table, pt.data(), pt.size() * 4, hipMemcpyHostToDevice), "page table upload");
+  HIPCHK(launch_rope_table((float2*)(c->kv + k.rope), max_tokens_per_seq, c->cfg.head_dim, c->cfg.rope_base,
+                           c->stream),
+         "rope table");
+  HIPCHK(hipStreamSynchronize(c->stream), "rope table");
+  c->n_kv.assign(n_seqs, 0);
+  c->kv_len.assign(n_seqs, std::vector<int32_t>(c->cfg.n_layers, 0));
+  c->mask.assign(n_seqs, std::vector<uint8_t>(c->cfg.n_layers, 0));
+  return TSS_OK;
+}
+
+int tss_set_skip_mask(tss_ctx* c, int32_t seq, const uint8_t* mask) {
+  if (!c) return TSS_EINVAL;
+  if (seq < 0 || seq >= c->n_seqs) return fail(c, TSS_EINVAL, "unknown sequence");
+  if (mask && !mask_ok(mask, c->cfg.n_layers)) return fail(c, TSS_EINVAL, "mask bytes must be 0 or 1");
+  for (int l = 0; l < c->cfg.n_layers; ++l) c->mask[seq][l] = mask ? mask[l] : 0;
+  return TSS_OK;
+}
+
+int tss_seq_length(tss_ctx* c, int32_t seq, int32_t* n_kv) {
+  if (!c || !n_kv) return TSS_EINVAL;
+  if (seq < 0 || seq >= c->n_seqs) return fail(c, TSS_EINVAL, "unknown sequence");
+  *n_kv = c->n_kv[seq];
+  return TSS_OK;
+}
+
+int tss_seq_truncate(tss_ctx* c, int32_t seq, int32_t n_kv) {
+  if (!c) return TSS_EINVAL;
+  if (seq < 0 || seq >= c->n_seqs) return fail(c, TSS_EINVAL, "unknown sequence");
+  if (n_kv < 0 || n_kv > c->n_kv[seq]) return fail(c, TSS_EINVAL, "truncate can only shorten a sequence");
+  c->n_kv[seq] = n_kv;
+  for (auto& k : c->kv_len[seq]) k = std::min(k, n_kv);
+  return TSS_OK;
+}
+
+int tss_profile_kernel(tss_ctx* c, int32_t kernel, int32_t layer) {
+  if (!c) return TSS_EINVAL;
+  if (kernel < -1 || kernel > TSS_K_COMPACT) return fail(c, TSS_EINVAL, "unknown kernel kind");
+  c->prof_kind = kernel;
+  c->prof_layer = layer;
+  return TSS_OK;
+}
+
+int tss_profile_read(tss_ctx* c, double* total_ms, int64_t* count, int32_t reset) {
+  if (!c) return TSS_EINVAL;
+  if (total_ms) *total_ms = c->prof_ms;
+  if (count) *count = c->prof_count;
+  if (reset) {
+    c->prof_ms = 0.0;
+    c->prof_count = 0;
+  }
+  return TSS_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Brackets one launch with events when it is the profiled one.
+struct ProfScope {
+  tss_ctx* c;
+  bool on;
+  ProfScope(tss_ctx* ctx, int kind, int layer) : c(ctx) {
+    on = c->prof_kind == kind && (layer < 0 || c->prof_layer == layer) && !c->prof_armed;
+    if (on) {
+      (void)hipEventRecord(c->ev0, c->stream);
+    }
+  }
+  void done() {
+    if (on) {
+      (void)hipEventRecord(c->ev1, c->stream);
+      c->prof_armed = true;
+    }
+  }
+};
+
+// Runs embed, the active blocks and (for verify) lm_head + accept for the
+// nodes already in c->sp_host.  seq's page table is used for KV.
+int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
+  const tss_model_cfg& cf = c->cfg;
+  const StepParams& sp = *c->sp_host;
+  const int M = sp.M, L = cf.n_layers, d = cf.d_model, f = cf.ffn_dim, H = cf.n_heads, hd = cf.head_dim;
+  const int mt = (M + 15) / 16;
+  uint8_t* ws = c->ws;
+  StepParams* sp_dev = (StepParams*)(ws + c->wsl.sp);
+  const int32_t* pt = (const int32_t*)(c->kv + c->kvl.page_table) + (size_t)seq * c->kvl.pages_per_seq;
+  uint8_t* pages = c->kv + c->kvl.pages;
+  const float2* rope = (const float2*)(c->kv + c->kvl.rope);
+  hipStream_t s = c->stream;
+
+  std::vector<int> active;
+  for (int l = 0; l < L; ++l)
+    if (!sp.mask[l]) active.push_back(l);
+  auto attn_gain = [&](int idx) -> const float* {
+    return (const float*)(c->w + (idx < (int)active.size() ? c->wl.layers[active[idx]].attn_norm : c->wl.final_norm));
+  };
+
+  c->prof_armed = false;
+  HIPCHK(hipMemcpyAsync(sp_dev, c->sp_host, sizeof(StepParams), hipMemcpyHostToDevice, s), "step params");
+
+  {
+    EmbedArgs a{};
+    a.embed = c->w + c->wl.embed;
+    a.sp = sp_dev;
+    a.gain = attn_gain(0);
+    a.h = (float*)(ws + c->wsl.h);
+    a.xn = ws + c->wsl.xa;
+    a.xn_plane = act_planes(&cf) == 2 ? (size_t)c->Mp * d : 0;
+    a.ss_out = (float*)(ws + c->wsl.ss_a);
+    a.d = d;
+    a.M = M;
+    a.Mp = c->Mp;
+    ProfScope ps(c, TSS_K_EMBED, -1);
+    HIPCHK(launch_embed(c->bf16, a, s), "embed");
+    ps.done();
+  }
+
+  GemmArgs base{};
+  base.M = M;
+  base.Mp = c->Mp;
+  const bool two = act_planes(&cf) == 2;
+  const size_t plane_d = two ? (size_t)c->Mp * d : 0, plane_f = two ? (size_t)c->Mp * f : 0;
+  base.eps = cf.rms_eps;
+  base.norm_dim = d;
+  base.sp = sp_dev;
+
+  // attention split: about 1024 waves over (split, head, node tile)
+  const int total = sp.n_kv + M;
+  const int n_pages = (total + kPage - 1) / kPage;
+  const int target = std::max(1, 1024 / (H * mt));
+  int pps = std::max(1, (n_pages + target - 1) / target);
+  while ((n_pages + pps - 1) / pps > kMaxSplit) ++pps;
+  const int nsplit = (n_pages + pps - 1) / pps;
+
+  for (size_t idx = 0; idx < active.size(); ++idx) {
+    const int l = active[idx];
+    const LayerW& W = c->wl.layers[l];
+    {  // RMSNorm + QKV + RoPE + KV append
+      GemmArgs a = base;
+      a.w = c->w + W.qkv;
+      a.x = ws + c->wsl.xa;
+      a.x_plane = plane_d;
+      a.K = d;
+      a.N = 3 * d;
+      a.nkc = d / c->KC;
+      a.ss_in = (const float*)(ws + c->wsl.ss_a);
+      a.ss_nparts = idx == 0 ? 1 : d / 16;
+      a.q = (float*)(ws + c->wsl.q);
+      a.kv_pages = pages;
+      a.page_table = pt;
+      a.rope = rope;
+      a.layer = l;
+      a.n_pages_pool = c->kvl.n_pages;
+      a.n_heads = H;
+      a.head_dim = hd;
+      a.d = d;
+      ProfScope ps(c, TSS_K_QKV, l);
+      HIPCHK(launch_gemm(c->bf16, EPI_QKV, mt, a, s), "qkv gemm");
+      ps.done();
+    }
+    {  // tree attention + split combine
+      AttnArgs a{};
+      a.q = (const float*)(ws + c->wsl.q);
+      a.kv_pages = pages;
+      a.page_table = pt;
+      a.sp = sp_dev;
+      a.part_o = (float*)(ws + c->wsl.part_o);
+      a.part_ml = (float*)(ws + c->wsl.part_ml);
+      a.layer = l;
+      a.n_pages_pool = c->kvl.n_pages;
+      a.n_heads = H;
+      a.d = d;
+      a.M = M;
+      a.Mp = c->Mp;
+      a.n_kv = sp.n_kv;
+      a.pages_per_split = pps;
+      a.nsplit = nsplit;
+      a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
+      ProfScope ps(c, TSS_K_ATTN, l);
+      HIPCHK(launch_attn(c->bf16, hd, mt, a, s), "attention");
+      CombineArgs cb{};
+      cb.part_o = a.part_o;
+      cb.part_ml = a.part_ml;
+      cb.o = ws + c->wsl.o;
+      cb.o_plane = plane_d;
+      cb.n_heads = H;
+      cb.d = d;
+      cb.M = M;
+      cb.Mp = c->Mp;
+      cb.nsplit = nsplit;
+      HIPCHK(launch_combine(c->bf16, hd, cb, s), "attention combine");
+      ps.done();
+    }
+    {  // O projection + residual; next norm input
+      GemmArgs a = base;
+      a.w = c->w + W.o;
+      a.x = ws + c->wsl.o;
+      a.x_plane = plane_d;
+      a.K = d;
+      a.N = d;
+      a.nkc = d / c->KC;
+      a.h = (float*)(ws + c->wsl.h);
+      a.xn = ws + c->wsl.xm;
+      a.xn_plane = plane_d;
+      a.g_next = (const float*)(c->w + W.mlp_norm);
+      a.ss_out = (float*)(ws + c->wsl.ss_m);
+      ProfScope ps(c, TSS_K_OPROJ, l);
+      HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, a, s), "o gemm");
+      ps.done();
+    }
+    {  // RMSNorm + gate/up + SwiGLU
+      GemmArgs a = base;
+      a.w = c->w + W.gateup;
+      a.x = ws + c->wsl.xm;
+      a.x_plane = plane_d;
+      a.K = d;
+      a.N = 2 * f;
+      a.nkc = d / c->KC;
+      a.ss_in = (const float*)(ws + c->wsl.ss_m);
+      a.ss_nparts = d / 16;
+      a.act = ws + c->wsl.act;
+      a.act_plane = plane_f;
+      ProfScope ps(c, TSS_K_GATEUP, l);
+      HIPCHK(launch_gemm(c->bf16, EPI_SWIGLU, mt, a, s), "gate/up gemm");
+      ps.done();
+    }
+    {  // down projection + residual; next norm input
+      GemmArgs a = base;
+      a.w = c->w + W.down;
+      a.x = ws + c->wsl.act;
+      a.x_plane = plane_f;
+      a.K = f;
+      a.N = d;
+      a.nkc = f / c->KC;
+      a.h = (float*)(ws + c->wsl.h);
+      a.xn = ws + c->wsl.xa;
+      a.xn_plane = plane_d;
+      a.g_next = attn_gain((int)idx + 1);
+      a.ss_out = (float*)(ws + c->wsl.ss_a);
+      ProfScope ps(c, TSS_K_DOWN, l);
+      HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, a, s), "down gemm");
+      ps.done();
+    }
+  }
+
+  if (verify) {
+    {  // final norm + lm_head + per-strip argmax
+      GemmArgs a = base;
+      a.w = c->w + c->wl.lm_head;
+      a.x = ws + c->wsl.xa;
+      a.x_plane = plane_d;
+      a.K = d;
+      a.N = cf.vocab;
+      a.nkc = d / c->KC;
+      a.ss_in = (const float*)(ws + c->wsl.ss_a);
+      a.ss_nparts = active.empty() ? 1 : d / 16;
+      a.logits = (float*)(ws + c->wsl.logits);
+      a.am_val = (float*)(ws + c->wsl.am_val);
+      a.am_idx = (int32_t*)(ws + c->wsl.am_idx);
+      ProfScope ps(c, TSS_K_LMHEAD, -1);
+      HIPCHK(launch_gemm(c->bf16, EPI_LOGITS, mt, a, s), "lm_head gemm");
+      ps.done();
+    }
+    {
+      AcceptArgs a{};
+      a.am_val = (const float*)(ws + c->wsl.am_val);
+      a.am_idx = (const int32_t*)(ws + c->wsl.am_idx);
+      a.nparts = cf.vocab / 16;
+      a.M = M;
+      a.Mp = c->Mp;
+      a.sp = sp_dev;
+      a.greedy = (int32_t*)(ws + c->wsl.greedy);
+      a.result = (Result*)(ws + c->wsl.result);
+      ProfScope ps(c, TSS_K_ACCEPT, -1);
+      HIPCHK(launch_accept(a, s), "accept");
+      ps.done();
+    }
+    if (compact) {
+      CompactArgs a{};
+      a.kv_pages = pages;
+      a.page_table = pt;
+      a.sp = sp_dev;
+      a.result = (const Result*)(ws + c->wsl.result);
+      a.n_layers = L;
+      a.n_pages_pool = c->kvl.n_pages;
+      a.n_heads = H;
+      a.head_dim = hd;
+      a.n_kv = sp.n_kv;
+      ProfScope ps(c, TSS_K_COMPACT, -1);
+      HIPCHK(launch_compact(c->bf16, a, s), "kv compaction");
+      ps.done();
+    }
+    HIPCHK(hipMemcpyAsync(c->res_host, ws + c->wsl.result, sizeof(Result), hipMemcpyDeviceToHost, s), "result copy");
+  }
+  HIPCHK(hipStreamSynchronize(s), "step");
+  if (c->prof_armed) {
+    float ms = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms, c->ev0, c->ev1), "event timing");
+    c->prof_ms += ms;
+    c->prof_count += 1;
+    c->prof_armed = false;
+  }
+  return TSS_OK;
+}
+
+int check_ready(tss_ctx* c, int seq) {
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  if (!c->kv) return fail(c, TSS_ESTATE, "no KV pool bound (tss_kv_alloc)");
+  if (seq < 0 || seq >= c->n_seqs) return fail(c, TSS_EINVAL, "unknown sequence");
+  return TSS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tss_prefill(tss_ctx* c, int32_t seq, const int32_t* tokens, int32_t n) {
+  if (!c) return TSS_EINVAL;
+  int r = check_ready(c, seq);
+  if (r) return r;
+  if (n < 0 || (n > 0 && !tokens)) return fail(c, TSS_EINVAL, "bad token array");
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= c->cfg.vocab) return fail(c, TSS_EINVAL, "token outside [0, vocab)");
+  if (c->n_kv[seq] + n > c->max_tokens) return fail(c, TSS_ECAPACITY, "prefill exceeds the sequence's KV capacity");
+  const int L = c->cfg.n_layers;
+  for (int l = 0; l < L; ++l)
+    if (!c->mask[seq][l] && c->kv_len[seq][l] != c->n_kv[seq])
+      return fail(c, TSS_ESTATE, "an active layer lacks K/V for the committed context");
+  const int chunk = std::min(c->cfg.max_nodes, kMaxNodes);
+  for (int done = 0; done < n; done += chunk) {
+    const int M = std::min(chunk, n - done);
+    StepParams& sp = *c->sp_host;
+    std::memset(&sp, 0, sizeof(sp));
+    sp.M = M;
+    sp.n_kv = c->n_kv[seq];
+    for (int i = 0; i < M; ++i) {
+      sp.tok[i] = tokens[done + i];
+      sp.parent[i] = i - 1;
+      sp.depth[i] = i;
+      sp.pos[i] = sp.n_kv + i;
+      sp.anc[i] = (i == 63) ? ~0ull : ((1ull << (i + 1)) - 1);
+    }
+    for (int l = 0; l < L; ++l) sp.mask[l] = c->mask[seq][l];
+    r = run_step(c, seq, false, false);
+    if (r) return r;
+    c->n_kv[seq] += M;
+    for (int l = 0; l < L; ++l)
+      if (!sp.mask[l]) c->kv_len[seq][l] = c->n_kv[seq];
+  }
+  return TSS_OK;
+}
+
+int tss_verify(tss_ctx* c, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent, int32_t n_nodes,
+               const uint8_t* skip_mask, uint32_t flags, int32_t* accept_len, int32_t* next_token) {
+  if (!c) return TSS_EINVAL;
+  int r = check_ready(c, seq);
+  if (r) return r;
+  if (!draft_tokens || !accept_len || !next_token) return fail(c, TSS_EINVAL, "null argument");
+  if (flags & ~(uint32_t)TSS_COMMIT) return fail(c, TSS_EINVAL, "unknown flag");
+  if (validate_tree(tree_parent, n_nodes, c->cfg.max_nodes) != TSS_OK)
+    return fail(c, TSS_EINVAL, "invalid draft tree (n_nodes, parent[0] = -1, 0 <= parent[i] < i)");
+  const int L = c->cfg.n_layers;
+  if (skip_mask && !mask_ok(skip_mask, L)) return fail(c, TSS_EINVAL, "mask bytes must be 0 or 1");
+  for (int i = 0; i < n_nodes; ++i)
+    if (draft_tokens[i] < 0 || draft_tokens[i] >= c->cfg.vocab) return fail(c, TSS_EINVAL, "token outside [0, vocab)");
+  const int n_kv = c->n_kv[seq];
+  if (n_kv + n_nodes > c->max_tokens) return fail(c, TSS_ECAPACITY, "verify exceeds the sequence's KV capacity");
+  const uint8_t* m = skip_mask ? skip_mask : c->mask[seq].data();
+  for (int l = 0; l < L; ++l)
+    if (!m[l] && c->kv_len[seq][l] != n_kv)
+      return fail(c, TSS_ESTATE, "an active layer lacks K/V for the committed context");
+
+  StepParams& sp = *c->sp_host;
+  std::memset(&sp, 0, sizeof(sp));
+  sp.M = n_nodes;
+  sp.n_kv = n_kv;
+  tree_meta(tree_parent, n_nodes, sp.depth, sp.anc);
+  for (int i = 0; i < n_nodes; ++i) {
+    sp.tok[i] = draft_tokens[i];
+    sp.parent[i] = tree_parent ? tree_parent[i] : i - 1;
+    sp.pos[i] = n_kv + sp.depth[i];
+  }
+  for (int l = 0; l < L; ++l) sp.mask[l] = m[l];
+  const bool commit = flags & TSS_COMMIT;
+  bool is_chain = true;
+  for (int i = 1; i < n_nodes; ++i)
+    if (sp.parent[i] != i - 1) is_chain = false;
+  r = run_step(c, seq, true, commit && !is_chain);
+  if (r) return r;
+  c->last_M = n_nodes;
+  *accept_len = c->res_host->accept_len;
+  *next_token = c->res_host->next_token;
+  if (commit) {
+    c->n_kv[seq] = n_kv + c->res_host->accept_len + 1;
+    for (int l = 0; l < L; ++l)
+      if (!m[l]) c->kv_len[seq][l] = c->n_kv[seq];
+  }
+  return TSS_OK;
+}
+
+int tss_get_logits(tss_ctx* c, float* host_dst, int32_t n_nodes) {
+  if (!c || !host_dst) return TSS_EINVAL;
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  if (n_nodes < 1 || n_nodes > c->last_M) return fail(c, TSS_EINVAL, "n_nodes exceeds the last verify's nodes");
+  HIPCHK(hipStreamSynchronize(c->stream), "sync");
+  HIPCHK(hipMemcpy(host_dst, c->ws + c->wsl.logits, (size_t)n_nodes * c->cfg.vocab * 4, hipMemcpyDeviceToHost),
+         "logits copy");
+  return TSS_OK;
+}
+
+int tss_get_greedy(tss_ctx* c, int32_t* host_dst, int32_t n_nodes) {
+  if (!c || !host_dst) return TSS_EINVAL;
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  if (n_nodes < 1 || n_nodes > c->last_M) return fail(c, TSS_EINVAL, "n_nodes exceeds the last verify's nodes");
+  HIPCHK(hipStreamSynchronize(c->stream), "sync");
+  HIPCHK(hipMemcpy(host_dst, c->ws + c->wsl.greedy, (size_t)n_nodes * 4, hipMemcpyDeviceToHost), "greedy copy");
+  return TSS_OK;
+}
+
+}  // extern "C"

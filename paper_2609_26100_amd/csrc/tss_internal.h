@@ -1,0 +1,186 @@
+// Internal definitions shared by the host runtime and the gfx950 kernels.
+//
+// Device data layout (all buffers owned by the caller):
+//
+//   packed weights  embed [V][d] (T, row-major, gathered by token id);
+//                   per layer: attn_norm [d] f32, W_qkv packed, W_o packed,
+//                   mlp_norm [d] f32, W_gateup packed, W_down packed;
+//                   final_norm [d] f32; lm_head packed.
+//                   A packed matrix W [N][K] is cut into 16-row x KC-column
+//                   tiles of exactly 1 KiB (KC = 32 for bf16, 16 for f32),
+//                   each stored in MFMA lane order: lane l's 16 bytes are row
+//                   (l % 16), columns (l / 16) * KC/4 .. + KC/4 of the tile.
+//                   NT adjacent row tiles form a strip; strips are stored one
+//                   after the other and, inside a strip, tiles interleave by
+//                   K chunk (chunk c of tile t sits at index c * NT + t), so a
+//                   wave streaming one strip reads NT KiB contiguous per chunk.
+//   workspace       step parameters, residual h [Mp][d] f32, GEMM input
+//                   activations, q, attention partials, logits, argmax
+//                   partials, greedy tokens, result (offsets in WsLayout).
+//   KV pool         page tables, the rotary cos/sin table, then pages.  One
+//                   page holds 16 tokens; for (layer, page, head) a K block
+//                   [16][hd] (token-major) and a V block [4][hd][4] (token
+//                   t at [t / 4][dim][t % 4]), each 16 * hd elements of KV.
+//
+// Precision modes (T = weight type):
+//   bf16  weights bf16.  GEMM input activations are fp32 values stored as two
+//         bf16 planes, hi = bf16(v) and lo = bf16(v - hi) (planes Mp*K
+//         elements apart); a pair of bf16 MFMAs against the same weight tile
+//         reproduces v * w to about 16 significant bits.  KV cache, q and the
+//         attention probabilities are fp16.  Accumulation, residual stream,
+//         norms, softmax and logits are fp32.
+//   f32   everything fp32 (one activation plane, fp32 KV).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tss {
+
+constexpr int kPage = 16;          // tokens per KV page
+constexpr int kMaxNodes = 64;      // nodes of one verify step (u64 ancestor masks)
+constexpr int kMaxLayers = 256;
+constexpr int kTileBytes = 1024;   // one packed 16 x KC weight tile
+
+template <typename T> struct Mode;
+template <> struct Mode<__bf16> {
+  using KV = _Float16;
+  static constexpr int planes = 2;
+};
+template <> struct Mode<float> {
+  using KV = float;
+  static constexpr int planes = 1;
+};
+
+// Stores an fp32 activation in the mode's plane format.
+template <typename T>
+__device__ __forceinline__ void store_act(void* base, size_t plane, size_t idx, float v) {
+  if constexpr (Mode<T>::planes == 2) {
+    const T hi = (T)v;
+    ((T*)base)[idx] = hi;
+    ((T*)base)[plane + idx] = (T)(v - (float)hi);
+  } else {
+    ((T*)base)[idx] = v;
+  }
+}
+
+struct StepParams {
+  int32_t M;                       // nodes in this step
+  int32_t n_kv;                    // committed context length
+  int32_t tok[kMaxNodes];
+  int32_t pos[kMaxNodes];          // n_kv + depth
+  int32_t parent[kMaxNodes];
+  int32_t depth[kMaxNodes];
+  uint64_t anc[kMaxNodes];         // bit j: node j is this node or an ancestor
+  uint8_t mask[kMaxLayers];        // 1 = block skipped in this step
+};
+
+struct Result {
+  int32_t accept_len;
+  int32_t next_token;
+  int32_t best;
+  int32_t path_len;                // accept_len + 1
+  int32_t path[kMaxNodes];         // node ids root -> best
+};
+
+enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+
+struct GemmArgs {
+  const uint8_t* w;        // packed weights of this matrix
+  const void* x;           // A operand rows [M][K] of T (row stride K), planes x_plane apart
+  size_t x_plane;
+  int M, K, N;             // N = packed output columns
+  int nkc;                 // K / KC
+  // RMSNorm of the A rows: x holds T(h * gain); the row scale
+  // rsqrt(sum(h^2) / norm_dim + eps) is applied to the products here.
+  const float* ss_in;      // [ss_nparts][Mp] partial sums of h^2 (null: no norm)
+  int ss_nparts;
+  int norm_dim;
+  float eps;
+  int Mp;                  // row stride of the partial-sum arrays
+  const StepParams* sp;
+  // EPI_QKV
+  float* q;                // [Mp][d]
+  uint8_t* kv_pages;       // first page of the pool
+  const int32_t* page_table;
+  const float2* rope;      // [max_pos][hd/2] (cos, sin)
+  int layer, n_pages_pool, n_heads, head_dim, d;
+  // EPI_RESID
+  float* h;                // [Mp][N] residual, updated in place
+  void* xn;                // [Mp][N] activation planes of h_new * g_next
+  size_t xn_plane;
+  const float* g_next;     // gain of the next RMSNorm
+  float* ss_out;           // [N / (16 NT)][Mp] partial sums of h_new^2
+  // EPI_SWIGLU
+  void* act;               // [Mp][N/2] activation planes of silu(gate) * up
+  size_t act_plane;
+  // EPI_LOGITS
+  float* logits;           // [Mp][N]
+  float* am_val;           // [N / (16 NT)][Mp]
+  int32_t* am_idx;
+};
+
+struct AttnArgs {
+  const float* q;          // [Mp][d]
+  const uint8_t* kv_pages;
+  const int32_t* page_table;
+  const StepParams* sp;
+  float* part_o;           // [H][nsplit][Mp][hd]
+  float* part_ml;          // [H][nsplit][Mp][2] (running max in log2 units, sum)
+  int layer, n_pages_pool, n_heads, d, M, Mp;
+  int n_kv, pages_per_split, nsplit;
+  float scale_log2;        // log2(e) / sqrt(hd)
+};
+
+struct CombineArgs {
+  const float* part_o;
+  const float* part_ml;
+  void* o;                 // [Mp][d] activation planes
+  size_t o_plane;
+  int n_heads, d, M, Mp, nsplit;
+};
+
+struct EmbedArgs {
+  const void* embed;       // [V][d] T
+  const StepParams* sp;
+  const float* gain;       // gain of the first RMSNorm the rows meet
+  float* h;                // [Mp][d]
+  void* xn;                // [Mp][d] activation planes
+  size_t xn_plane;
+  float* ss_out;           // [1][Mp]
+  int d, M, Mp;
+};
+
+struct AcceptArgs {
+  const float* am_val;     // [nparts][Mp]
+  const int32_t* am_idx;
+  int nparts, M, Mp;
+  const StepParams* sp;
+  int32_t* greedy;         // [Mp]
+  Result* result;
+};
+
+struct CompactArgs {
+  uint8_t* kv_pages;
+  const int32_t* page_table;
+  const StepParams* sp;
+  const Result* result;
+  int n_layers, n_pages_pool, n_heads, head_dim, n_kv;
+};
+
+// Launchers (defined in the .hip files).  T is selected by `bf16`.
+hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_t s);
+hipError_t launch_attn(bool bf16, int head_dim, int qt, const AttnArgs& a, hipStream_t s);
+hipError_t launch_combine(bool bf16, int head_dim, const CombineArgs& a, hipStream_t s);
+hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s);
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+hipError_t launch_compact(bool bf16, const CompactArgs& a, hipStream_t s);
+hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base, hipStream_t s);
+
+// Strip width (16-row tiles per strip) of a packed matrix: gate and up tiles
+// pair up so one workgroup sees both halves of SwiGLU; every other matrix
+// uses single-tile strips.
+inline int strip_tiles(int epi) { return epi == EPI_SWIGLU ? 2 : 1; }
+
+}  // namespace tss

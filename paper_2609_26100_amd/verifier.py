@@ -1,0 +1,73 @@
+"""A TSS verifier bound to torch-owned device buffers.
+
+PyTorch only provides the device memory (packed weights, workspace, KV pool)
+and the HIP stream; every step of the verify path runs in libtss.so.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import tss as abi
+
+
+class Verifier:
+    def __init__(self, shape, n_seqs=1, max_tokens=2048, max_nodes=64, device="cuda:0", stream=None,
+                 page_order=None):
+        import torch
+
+        self.torch = torch
+        self.shape = shape
+        self.device = torch.device(device)
+        self.cfg = abi.make_cfg(shape, max_nodes)
+        if abi.tss_cfg_check(self.cfg) != abi.TSS_OK:
+            raise ValueError(f"unsupported shape {shape}")
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        wb = abi.tss_weights_bytes(self.cfg)
+        sb = abi.tss_workspace_bytes(self.cfg)
+        kb = abi.tss_kv_bytes(self.cfg, n_seqs, max_tokens)
+        self.weights = torch.empty(wb, dtype=torch.uint8, device=self.device)
+        self.workspace = torch.zeros(sb, dtype=torch.uint8, device=self.device)
+        self.kv_pool = torch.zeros(kb, dtype=torch.uint8, device=self.device)
+        torch.cuda.synchronize(self.device)
+        self.ctx = abi.tss_create(self.cfg, self.stream.cuda_stream, self.weights.data_ptr(), wb,
+                                  self.workspace.data_ptr(), sb)
+        abi.tss_kv_alloc(self.ctx, n_seqs, max_tokens, self.kv_pool.data_ptr(), kb, page_order)
+        self.n_seqs, self.max_tokens = n_seqs, max_tokens
+
+    def load(self, get_tensor):
+        """Streams every tensor, in the ABI's tensor order, from get_tensor(index) -> host array in the
+        shape's dtype (fp32, or bf16 bit patterns as uint16)."""
+        for idx in range(3 + 9 * self.shape.n_layers):
+            abi.tss_load_weights(self.ctx, idx, [get_tensor(idx)])
+
+    def set_mask(self, seq, mask):
+        abi.tss_set_skip_mask(self.ctx, seq, mask)
+
+    def prefill(self, seq, tokens):
+        abi.tss_prefill(self.ctx, seq, tokens)
+
+    def verify(self, seq, tokens, parent=None, mask=None, commit=False):
+        return abi.tss_verify(self.ctx, seq, tokens, parent, mask, abi.TSS_COMMIT if commit else 0)
+
+    def logits(self, n_nodes):
+        return abi.tss_get_logits(self.ctx, n_nodes, self.shape.vocab)
+
+    def greedy(self, n_nodes):
+        return abi.tss_get_greedy(self.ctx, n_nodes)
+
+    def length(self, seq):
+        return abi.tss_seq_length(self.ctx, seq)
+
+    def truncate(self, seq, n):
+        abi.tss_seq_truncate(self.ctx, seq, n)
+
+    def close(self):
+        if self.ctx:
+            abi.tss_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

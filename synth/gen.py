@@ -238,3 +238,15 @@ def random_skip_mask(n_layers: int, lo: int, hi: int, count: int, seed: int = BA
     rng = _rng(_P_MASK, n_layers, lo, hi, stream, count + 1000, seed=seed)
     layers = rng.choice(np.arange(lo, hi + 1), size=count, replace=False)
     return mask_from_layers(n_layers, layers)
+
+
+def abi_tensor_loader(shape, seed: int = BASE_SEED, random_gains: bool = False):
+    """get_tensor(index) for the library's load order: fp32 arrays, or bf16
+    bit patterns (uint16) for bf16 shapes."""
+    names = {i: (layer, nm) for i, layer, nm in tensor_names(shape.n_layers)}
+
+    def get(index):
+        layer, nm = names[index]
+        return weight_tensor(shape, nm, layer, seed=seed, random_gains=random_gains,
+                             as_bf16_bits=shape.dtype == "bf16")
+    return get

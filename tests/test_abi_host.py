@@ -1,0 +1,126 @@
+"""Host side of the C ABI, on the CPU: the library loads, exports every function
+include/tss.h declares, and its pure host checks (config, tree, mask, tree
+metadata, size queries, argument validation before any device work) behave as
+documented.  No compute call is made here."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import tree_meta as oracle_tree_meta
+from paper_2609_26100_amd import tss as abi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "tss.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tss_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = abi.lib()
+    declared = _declared()
+    assert len(declared) >= 20
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(abi.EXPORTS) == declared
+
+
+@pytest.mark.parametrize("shape", [synth.TINY, synth.LLAMA_7B, synth.LLAMA_13B, synth.LLAMA_33B])
+def test_cfg_accepts_workload_shapes(shape):
+    cfg = abi.make_cfg(shape)
+    assert abi.tss_cfg_check(cfg) == abi.TSS_OK
+    wb = abi.tss_weights_bytes(cfg)
+    es = 2 if shape.dtype == "bf16" else 4
+    d, f, v, L = shape.d_model, shape.ffn_dim, shape.vocab, shape.n_layers
+    params = 2 * v * d + L * (4 * d * d + 3 * d * f)
+    assert params * es <= wb <= params * es + (L * 6 + 3) * 256 + (2 * L + 1) * d * 4
+    assert abi.tss_workspace_bytes(cfg) > 0
+    kb = abi.tss_kv_bytes(cfg, 1, 1030)
+    assert kb >= L * 65 * 16 * 2 * d * es
+
+
+def test_7b_sizes():
+    cfg = abi.make_cfg(synth.LLAMA_7B)
+    assert abs(abi.tss_weights_bytes(cfg) - 13.48e9) < 0.02e9
+
+
+@pytest.mark.parametrize("field,val", [("head_dim", 96), ("d_model", 4000), ("vocab", 32001), ("max_nodes", 65),
+                                       ("max_nodes", 0), ("n_layers", 0), ("dtype", 7), ("rms_eps", 0.0),
+                                       ("ffn_dim", 11000), ("n_layers", 257)])
+def test_cfg_rejects(field, val):
+    cfg = abi.make_cfg(synth.LLAMA_7B)
+    setattr(cfg, field, val)
+    assert abi.tss_cfg_check(cfg) == abi.TSS_EINVAL
+    assert abi.tss_weights_bytes(cfg) == 0
+
+
+def test_validate_tree():
+    ok = [-1, 0, 0, 1, 3]
+    assert abi.tss_validate_tree(ok, 5, 64) == abi.TSS_OK
+    assert abi.tss_validate_tree(None, 6, 64) == abi.TSS_OK       # chain
+    for bad, n in (([0, 0], 2), ([-1, 1], 2), ([-1, 0, 2], 3), ([-1, -1], 2), ([-1, 0, 5], 3)):
+        assert abi.tss_validate_tree(bad, n, 64) == abi.TSS_EINVAL, bad
+    assert abi.tss_validate_tree(None, 0, 64) == abi.TSS_EINVAL
+    assert abi.tss_validate_tree(None, 65, 64) == abi.TSS_EINVAL
+    assert abi.tss_validate_tree(None, 7, 6) == abi.TSS_EINVAL
+
+
+def test_validate_mask():
+    assert abi.tss_validate_mask(np.array([0, 1, 0, 1], np.uint8), 4) == abi.TSS_OK
+    assert abi.tss_validate_mask(None, 4) == abi.TSS_OK
+    assert abi.tss_validate_mask(np.array([0, 2, 0, 1], np.uint8), 4) == abi.TSS_EINVAL
+    assert abi.tss_validate_mask(np.zeros(300, np.uint8), 300) == abi.TSS_EINVAL
+
+
+@pytest.mark.parametrize("n,stream", [(1, 0), (8, 1), (33, 2), (64, 3)])
+def test_tree_meta_matches_oracle(n, stream):
+    parent = synth.random_tree(n, seed=5, stream=stream)
+    st, depth, anc = abi.tss_tree_meta(parent, n)
+    assert st == abi.TSS_OK
+    od, vis = oracle_tree_meta(parent)
+    np.testing.assert_array_equal(depth, od)
+    for i in range(n):
+        bits = {j for j in range(n) if (int(anc[i]) >> j) & 1}
+        assert bits == vis[i]
+
+
+def test_tree_meta_chain_default():
+    st, depth, anc = abi.tss_tree_meta(None, 64)
+    assert st == abi.TSS_OK
+    assert list(depth) == list(range(64))
+    assert int(anc[63]) == (1 << 64) - 1
+
+
+def test_create_validates_before_device_work():
+    cfg = abi.make_cfg(synth.TINY)
+    L = abi.lib()
+    out = ctypes.c_void_p()
+    # null buffers
+    assert L.tss_create(ctypes.byref(cfg), None, None, 0, None, 0, ctypes.byref(out)) == abi.TSS_EINVAL
+    # buffers smaller than the size queries
+    assert L.tss_create(ctypes.byref(cfg), None, 0x1000, 16, 0x2000, 16, ctypes.byref(out)) == abi.TSS_ENOSPACE
+    assert out.value is None
+    bad = abi.make_cfg(synth.TINY)
+    bad.head_dim = 32
+    assert L.tss_create(ctypes.byref(bad), None, 0x1000, 1 << 40, 0x2000, 1 << 40, ctypes.byref(out)) == abi.TSS_EINVAL
+
+
+def test_null_context_calls_fail_cleanly():
+    L = abi.lib()
+    al, nt = ctypes.c_int32(), ctypes.c_int32()
+    assert L.tss_verify(None, 0, None, None, 1, None, 0, ctypes.byref(al), ctypes.byref(nt)) == abi.TSS_EINVAL
+    assert L.tss_prefill(None, 0, None, 0) == abi.TSS_EINVAL
+    assert L.tss_set_skip_mask(None, 0, None) == abi.TSS_EINVAL
+    assert L.tss_load_weights(None, 0, 1, None) == abi.TSS_EINVAL
+    L.tss_destroy(None)
+
+
+def test_status_strings():
+    for s in (abi.TSS_OK, abi.TSS_EINVAL, abi.TSS_ENOSPACE, abi.TSS_ECAPACITY, abi.TSS_ESTATE, abi.TSS_EHIP):
+        assert abi.tss_status_string(s) not in ("", "unknown status")

@@ -1,0 +1,225 @@
+"""GPU parity on the tiny fp32 decoder (4 layers, d 256, 4 heads x 64, FFN 704,
+vocab 4096): every kernel of the verify path against the oracle, element by
+element, plus the properties that must hold bit-exactly on the GPU."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import OracleSequence, prefill, verify
+from tests.gpu_common import compare_step, gpu_verifier, log, oracle_model
+
+pytestmark = pytest.mark.gpu
+
+SHAPE = synth.TINY
+L = SHAPE.n_layers
+
+
+@pytest.fixture(scope="module")
+def pair():
+    log("building tiny fp32 verifier (random gains)")
+    v = gpu_verifier(SHAPE, random_gains=True, n_seqs=4, max_tokens=600, max_nodes=64)
+    m = oracle_model(SHAPE, random_gains=True)
+    yield v, m
+    v.close()
+
+
+def _fresh(v, m, seq, mask, ctx):
+    v.truncate(seq, 0)
+    v.set_mask(seq, mask)
+    v.prefill(seq, ctx)
+    o = OracleSequence(m, mask)
+    prefill(m, o, ctx)
+    assert v.length(seq) == o.n_kv == len(ctx)
+    return o
+
+
+def test_all_blocks_skipped(pair):
+    v, m = pair
+    mask = np.ones(L, np.uint8)
+    ctx = synth.context_tokens(SHAPE.vocab, 20, stream=1)
+    o = _fresh(v, m, 0, mask, ctx)
+    tok = synth.context_tokens(SHAPE.vocab, 6, stream=2)
+    _, _, err, _ = compare_step(SHAPE, v, 0, m, o, tok)
+    log(f"all skipped: logits err {err:.2e}")
+
+
+@pytest.mark.parametrize("skip", [[], [0], [3], [1, 2], [0, 1, 3]])
+def test_masks_chain(pair, skip):
+    v, m = pair
+    mask = synth.mask_from_layers(L, skip)
+    ctx = synth.context_tokens(SHAPE.vocab, 57, stream=3)
+    o = _fresh(v, m, 1, mask, ctx)
+    tok = synth.context_tokens(SHAPE.vocab, 6, stream=4)
+    _, _, err, _ = compare_step(SHAPE, v, 1, m, o, tok)
+    log(f"mask {skip}: logits err {err:.2e}")
+
+
+def test_tiny_workload(pair):
+    """128 context tokens in KV, root, chain k=5 (3 greedy then 2 other tokens), mask {2}."""
+    v, m = pair
+    mask = synth.mask_from_layers(L, [2])
+    toks = synth.context_tokens(SHAPE.vocab, 129)
+    ctx, root = toks[:128], int(toks[128])
+    o = _fresh(v, m, 0, mask, ctx)
+    g, cur = [], [root]
+    for _ in range(5):
+        g.append(int(verify(m, o, np.asarray(cur)).greedy[-1]))
+        cur.append(g[-1])
+    drafts = synth.chain_draft(np.asarray(g), SHAPE.vocab, n_greedy=3)
+    res, (al, nt), err, compared = compare_step(SHAPE, v, 0, m, o, np.concatenate([[root], drafts]))
+    log(f"tiny workload: accept {al} next {nt} (oracle {res.accept_len} {res.next_token}) err {err:.2e}")
+    assert res.accept_len == 3 and compared
+
+
+@pytest.mark.parametrize("n_nodes", [1, 2, 8, 17, 33, 64])
+def test_trees(pair, n_nodes):
+    v, m = pair
+    mask = synth.mask_from_layers(L, [1])
+    ctx = synth.context_tokens(SHAPE.vocab, 45, stream=5)
+    o = _fresh(v, m, 2, mask, ctx)
+    parent = synth.random_tree(n_nodes, stream=n_nodes, max_children=4)
+    tok = synth.context_tokens(SHAPE.vocab, n_nodes, stream=6 + n_nodes)
+    _, _, err, _ = compare_step(SHAPE, v, 2, m, o, tok, parent)
+    log(f"tree {n_nodes}: logits err {err:.2e}")
+
+
+def test_prefill_chunks_and_context_lengths(pair):
+    """Contexts that end inside and at page edges, prefilled in several chunks."""
+    v, m = pair
+    for n in (1, 15, 16, 17, 64, 65, 200):
+        ctx = synth.context_tokens(SHAPE.vocab, n, stream=100 + n)
+        o = _fresh(v, m, 3, np.zeros(L, np.uint8), ctx)
+        tok = synth.context_tokens(SHAPE.vocab, 3, stream=200 + n)
+        _, _, err, _ = compare_step(SHAPE, v, 3, m, o, tok)
+        log(f"context {n}: logits err {err:.2e}")
+
+
+def test_tree_commit_then_chain(pair):
+    v, m = pair
+    mask = synth.mask_from_layers(L, [3])
+    ctx = synth.context_tokens(SHAPE.vocab, 31, stream=7)
+    o = _fresh(v, m, 1, mask, ctx)
+    parent = np.array([-1, 0, 0, 1, 2, 2, 4, 4, 6], dtype=np.int32)
+    # tokens along 0 -> 2 -> 5 follow the oracle's greedy choices so the accepted path is not a prefix
+    tok = np.array([int(synth.context_tokens(SHAPE.vocab, 1, stream=8)[0])] + [0] * 8, dtype=np.int64)
+    g = verify(m, o, tok[:1]).greedy
+    tok[1], tok[2] = (g[0] + 1) % SHAPE.vocab, g[0]
+    res = verify(m, o, tok[:3], parent[:3])
+    tok[3], tok[4] = 11, (res.greedy[2] + 3) % SHAPE.vocab
+    tok[5] = res.greedy[2]
+    res = verify(m, o, tok[:6], parent[:6])
+    tok[6], tok[7], tok[8] = res.greedy[4], 12, 13
+    res, (al, nt), err, compared = compare_step(SHAPE, v, 1, m, o, tok, parent, commit=True)
+    assert compared and res.path == [0, 2, 5] and al == 2
+    assert v.length(1) == o.n_kv == 31 + 3
+    nxt = np.concatenate([[nt], synth.context_tokens(SHAPE.vocab, 4, stream=9)])
+    _, _, err2, _ = compare_step(SHAPE, v, 1, m, o, nxt)
+    log(f"tree commit: errs {err:.2e} {err2:.2e}")
+
+
+def test_chain_as_tree_is_bit_exact(pair):
+    v, m = pair
+    ctx = synth.context_tokens(SHAPE.vocab, 40, stream=10)
+    _fresh(v, m, 0, np.zeros(L, np.uint8), ctx)
+    tok = synth.context_tokens(SHAPE.vocab, 7, stream=11)
+    a = v.verify(0, tok)
+    la = v.logits(7)
+    b = v.verify(0, tok, np.arange(-1, 6, dtype=np.int32))
+    lb = v.logits(7)
+    assert a == b
+    np.testing.assert_array_equal(la, lb)
+
+
+def test_run_to_run_bit_exact(pair):
+    v, m = pair
+    ctx = synth.context_tokens(SHAPE.vocab, 70, stream=12)
+    _fresh(v, m, 0, synth.mask_from_layers(L, [0]), ctx)
+    tok = synth.context_tokens(SHAPE.vocab, 20, stream=13)
+    parent = synth.random_tree(20, stream=14)
+    outs = []
+    for _ in range(3):
+        v.verify(0, tok, parent)
+        outs.append(v.logits(20))
+    np.testing.assert_array_equal(outs[0], outs[1])
+    np.testing.assert_array_equal(outs[0], outs[2])
+
+
+def test_page_permutation_is_bit_exact(pair):
+    v, m = pair
+    ctx = synth.context_tokens(SHAPE.vocab, 90, stream=15)
+    tok = synth.context_tokens(SHAPE.vocab, 6, stream=16)
+    _fresh(v, m, 0, np.zeros(L, np.uint8), ctx)
+    v.verify(0, tok)
+    ref = v.logits(6)
+    n_pages = 4 * ((600 + 15) // 16)
+    order = np.random.default_rng(3).permutation(n_pages).astype(np.int32)
+    w = gpu_verifier(SHAPE, random_gains=True, n_seqs=4, max_tokens=600, max_nodes=64, page_order=order)
+    w.prefill(0, ctx)
+    w.verify(0, tok)
+    np.testing.assert_array_equal(w.logits(6), ref)
+    w.close()
+
+
+def test_skip_equals_deleted_block_bit_exact(pair):
+    """GPU with mask {l} is bit-identical to the GPU on the model with block l deleted."""
+    v, m = pair
+    l = 2
+    short = dataclasses.replace(SHAPE, n_layers=L - 1)
+    short_names = {i: (ly, nm) for i, ly, nm in synth.tensor_names(L - 1)}
+
+    def get_short(idx):
+        ly, nm = short_names[idx]
+        return synth.weight_tensor(SHAPE, nm, ly + 1 if ly >= l else ly, random_gains=True)
+    from paper_2609_26100_amd.verifier import Verifier
+    w = Verifier(short, n_seqs=1, max_tokens=600, max_nodes=64)
+    w.load(get_short)
+    ctx = synth.context_tokens(SHAPE.vocab, 50, stream=17)
+    tok = synth.context_tokens(SHAPE.vocab, 9, stream=18)
+    parent = synth.random_tree(9, stream=19)
+    _fresh(v, m, 0, synth.mask_from_layers(L, [l]), ctx)
+    a = v.verify(0, tok, parent)
+    w.prefill(0, ctx)
+    b = w.verify(0, tok, parent)
+    assert a == b
+    np.testing.assert_array_equal(v.logits(9), w.logits(9))
+    w.close()
+
+
+def test_own_greedy_drafts_fully_accepted(pair):
+    v, m = pair
+    ctx = synth.context_tokens(SHAPE.vocab, 33, stream=20)
+    _fresh(v, m, 0, synth.mask_from_layers(L, [1]), ctx)
+    cur = [int(synth.context_tokens(SHAPE.vocab, 1, stream=21)[0])]
+    for _ in range(6):
+        v.verify(0, cur)
+        cur.append(int(v.greedy(len(cur))[-1]))
+    al, nt = v.verify(0, cur[:6])
+    assert al == 5 and nt == cur[6]
+
+
+def test_errors_leave_state_unchanged(pair):
+    from paper_2609_26100_amd import tss as abi
+    v, m = pair
+    ctx = synth.context_tokens(SHAPE.vocab, 10, stream=22)
+    _fresh(v, m, 0, synth.mask_from_layers(L, [2]), ctx)
+    with pytest.raises(abi.TSSError) as e:   # layer 2 has no KV for the context
+        v.verify(0, [1, 2], mask=np.zeros(L, np.uint8))
+    assert e.value.status == abi.TSS_ESTATE
+    with pytest.raises(abi.TSSError) as e:
+        v.verify(0, [1, SHAPE.vocab])
+    assert e.value.status == abi.TSS_EINVAL
+    with pytest.raises(abi.TSSError) as e:
+        v.verify(0, [1, 2, 3], [-1, 0, 2])
+    assert e.value.status == abi.TSS_EINVAL
+    with pytest.raises(abi.TSSError) as e:
+        v.verify(0, list(range(65)))
+    assert e.value.status == abi.TSS_EINVAL
+    with pytest.raises(abi.TSSError) as e:
+        v.prefill(0, np.zeros(600, np.int32))
+    assert e.value.status == abi.TSS_ECAPACITY
+    assert v.length(0) == 10
+    # still usable
+    v.verify(0, [1, 2], commit=True)
+    assert v.length(0) in (11, 12)
