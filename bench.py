@@ -63,15 +63,33 @@ def run_gpu(args):
     M = K_DRAFT + 1
     t0 = time.time()
     v = Verifier(shape, n_seqs=1, max_tokens=CTX + 64, max_nodes=64, device="cuda:0")
-    v.load(synth.abi_tensor_loader(shape))
-    log(f"weights generated and loaded in {time.time() - t0:.1f}s")
+    gen = synth.abi_tensor_loader(shape)
+    t_gen = [0.0]
+
+    def get(idx):
+        a = time.time()
+        arr = gen(idx)
+        t_gen[0] += time.time() - a
+        return arr
+    v.load(get)
+    log(f"weights generated ({t_gen[0]:.1f}s) and loaded ({time.time() - t0 - t_gen[0]:.1f}s)")
     toks = synth.context_tokens(shape.vocab, CTX + 1)
     ctx, root = toks[:CTX], int(toks[CTX])
     masks = synth.nested_skip_masks(shape.n_layers, 16, 31, SKIPS)
 
+    if args.calib_copy:
+        # a plain device copy of known size, so HBM counters can be scaled
+        n = int(args.calib_copy * (1 << 30))
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {n} bytes read, {n} bytes written")
+        del src, dst
+
     results = {}
     prof = None
-    for s in SKIPS:
+    for s in args.skips:
         mask = masks[s]
         v.truncate(0, 0)
         v.set_mask(0, mask)
@@ -92,6 +110,7 @@ def run_gpu(args):
         if s == 0:
             abi.tss_profile_kernel(v.ctx, abi.TSS_K_GATEUP, 0)
             abi.tss_profile_read(v.ctx, reset=True)
+        log(f"skip {s}: timing {args.steps} steps")
         torch.cuda.synchronize()
         lat = np.empty(args.steps)
         acc = np.empty(args.steps, dtype=np.int64)
@@ -125,8 +144,8 @@ def run_gpu(args):
         }
         log(f"skip {s}: median {med * 1e6:.0f} us, accepted {results[s]['accepted_tok_s']:.0f} tok/s, "
             f"roofline frac {results[s]['roofline_frac']:.3f}")
-    d0 = results[0]
-    for s in SKIPS[1:]:
+    d0 = results[args.skips[0]]
+    for s in args.skips[1:]:
         results[s]["latency_ratio_vs_dense"] = results[s]["latency_us_median"] / d0["latency_us_median"]
         results[s]["byte_ratio_vs_dense"] = results[s]["algorithmic_GB"] / d0["algorithmic_GB"]
     v.close()
@@ -193,7 +212,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-reps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--skips", default="0,4,8", help="skip counts to time; the first is the headline")
+    ap.add_argument("--calib-copy", type=float, default=0.0,
+                    help="GiB of a plain device copy run first (HBM counter calibration)")
     args = ap.parse_args()
+    args.skips = [int(x) for x in args.skips.split(",")]
+    if args.skips[0] != 0 or any(x not in SKIPS for x in args.skips):
+        raise SystemExit(f"--skips must start with 0 and use counts from {SKIPS}")
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
               "(the verify step runs on a single MI355X)", file=sys.stderr)
@@ -228,7 +253,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": "7B-shape decoder, chain k=5 (p=0.6), 1024-token paged context, dense mask",
                    "context": CTX, "k": K_DRAFT, "p_accept": P_ACCEPT, "page_tokens": 16,
-                   "skip_counts": list(SKIPS), "parallelism": "single GPU"},
+                   "skip_counts": args.skips, "parallelism": "single GPU"},
         "latency_us_median": d0["latency_us_median"],
         "step_roofline_frac": d0["roofline_frac"],
         "roofline": roof,

@@ -6,10 +6,12 @@
 // This is the attention half of an active block; bypassed blocks never reach
 // this kernel (Domain-Aware Skip Controller, block rule).
 //
-// One wavefront owns (KV split, head, 16-node tile) and walks its pages:
-//   * K page block [16 tokens][hd] is read with one contiguous 64-byte run per
-//     lane (the whole 4 KiB block per wave), and S = K Q^T comes out of MFMA
-//     with tokens on the rows and nodes on the columns.
+// G workgroups of 16 waves share (head, 16-node tile); wave w of workgroup g
+// walks pages 16 g + w, 16 (g + G) + w, ..., loading the next page while it
+// computes the current one:
+//   * The K page block [16 tokens][hd] is read with one contiguous 64-byte run
+//     per lane (the whole 4 KiB block per wave), and S = K Q^T comes out of
+//     MFMA with tokens on the rows and nodes on the columns.
 //   * The S accumulator layout (lane: node column, 4 token rows) is exactly
 //     the A-operand layout of the P V product, so probabilities never leave
 //     registers.  The V block is stored [4][hd][4] so each lane's B operand for
@@ -18,8 +20,12 @@
 //   * Operands: fp16 K/V pages, q and probabilities with fp32 accumulation
 //     (v_mfma_f32_16x16x32_f16 for S, v_mfma_f32_16x16x16_f16 for P V) in the
 //     bf16 mode; fp32 throughout (v_mfma_f32_16x16x4_f32) in the f32 mode.
-// Splits write (max, sum, unnormalised output) partials; k_combine merges them
-// in a fixed order, so results are bit-reproducible.
+// The 16 waves' softmax states meet in LDS (fixed order).  With G = 1 the
+// workgroup writes the normalised rows itself.  With G > 1 each workgroup
+// writes its partial state, releases it, and bumps a per-(head, tile)
+// counter; the last to arrive merges the G partials in workgroup order and
+// resets the counter.  No second kernel (a kernel boundary costs about 3 us
+// on this GPU) and bit-reproducible results.
 #include "tss_internal.h"
 
 namespace tss {
@@ -33,45 +39,47 @@ __device__ __forceinline__ unsigned pack_f16x2(float lo, float hi) {
   return (unsigned)__builtin_bit_cast(unsigned short, a) | ((unsigned)__builtin_bit_cast(unsigned short, b) << 16);
 }
 
-// T = KV element type (_Float16 or float).
-template <typename T, int HD>
-__global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
-  constexpr int DL = HD / 4;                    // dims per lane group in Q K^T
-  constexpr int NQ = DL * (int)sizeof(T) / 16;  // 16-byte K/Q chunks per lane
-  constexpr int NO = HD / 16;                   // output tiles of P V
-  constexpr int NV = NO * 4 * (int)sizeof(T) / 16;  // 16-byte V chunks per lane
+constexpr int kAttnWaves = 16;
 
-  const int split = blockIdx.x, head = blockIdx.y, qt = blockIdx.z;
-  const int lane = threadIdx.x, r16 = lane & 15, grp = lane >> 4;
+// TK = KV element type (_Float16 or float); TW = weight type of the mode
+// (selects the activation plane format of the output).
+template <typename TK, typename TW, int HD>
+__global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
+  constexpr int DL = HD / 4;                         // dims per lane group in Q K^T
+  constexpr int NQ = DL * (int)sizeof(TK) / 16;      // 16-byte K/Q chunks per lane
+  constexpr int NO = HD / 16;                        // output tiles of P V
+  constexpr int NV = NO * 4 * (int)sizeof(TK) / 16;  // 16-byte V chunks per lane
+  constexpr int W = kAttnWaves;
+
+  const int head = blockIdx.x, qt = blockIdx.y, g = blockIdx.z, G = gridDim.z;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r16 = lane & 15, grp = lane >> 4;
   const int M = a.M, n_kv = a.n_kv;
   const int qn = qt * 16 + r16;
 
   // B operand of S = K Q^T: lane (node qn, group grp) holds q[qn][head*HD + grp*DL + 0..DL).
-  uint4 qreg[NQ];
-  {
+  // Every wave uses the same tile, so wave 0 builds it once in LDS and the
+  // waves read it back per page instead of holding it in registers.
+  extern __shared__ float smem[];
+  uint4* sm_q = (uint4*)smem;              // [64][NQ]
+  if (wave == 0) {
     const float* qrow = a.q + (size_t)qn * a.d + head * HD + grp * DL;
 #pragma unroll
     for (int c = 0; c < NQ; ++c) {
+      uint4 qv = uint4{0, 0, 0, 0};
       if (qn < M) {
-        if constexpr (sizeof(T) == 2) {
+        if constexpr (sizeof(TK) == 2) {
           const float4 f0 = *(const float4*)(qrow + c * 8);
           const float4 f1 = *(const float4*)(qrow + c * 8 + 4);
-          qreg[c] = uint4{pack_f16x2(f0.x, f0.y), pack_f16x2(f0.z, f0.w), pack_f16x2(f1.x, f1.y),
-                          pack_f16x2(f1.z, f1.w)};
+          qv = uint4{pack_f16x2(f0.x, f0.y), pack_f16x2(f0.z, f0.w), pack_f16x2(f1.x, f1.y), pack_f16x2(f1.z, f1.w)};
         } else {
-          qreg[c] = *(const uint4*)(qrow + c * 4);
+          qv = *(const uint4*)(qrow + c * 4);
         }
-      } else {
-        qreg[c] = uint4{0, 0, 0, 0};
       }
+      sm_q[lane * NQ + c] = qv;
     }
   }
   const uint64_t anc = qn < M ? a.sp->anc[qn] : 0ull;
-
-  const int total = n_kv + M;
-  const int n_pages = (total + kPage - 1) / kPage;
-  const int p0 = split * a.pages_per_split;
-  const int p1 = min(p0 + a.pages_per_split, n_pages);
+  const int n_pages = (n_kv + M + kPage - 1) / kPage;
 
   float m_run = -1e30f, l_run = 0.f;
   f32x4 O[NO];
@@ -79,29 +87,40 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
   for (int n = 0; n < NO; ++n) O[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const size_t blk_elems = 16 * (size_t)HD;
-  for (int p = p0; p < p1; ++p) {
+  auto load_page = [&](int p, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
     const int phys = a.page_table[p];
-    const T* kb = (const T*)a.kv_pages + (((size_t)a.layer * a.n_pages_pool + phys) * 2 * a.n_heads + head) * blk_elems;
-    const T* vb = kb + (size_t)a.n_heads * blk_elems;
-    uint4 kreg[NQ], vreg[NV];
+    const TK* kb = (const TK*)a.kv_pages + (((size_t)a.layer * a.n_pages_pool + phys) * 2 * a.n_heads + head) * blk_elems;
+    const TK* vb = kb + (size_t)a.n_heads * blk_elems;
     const uint4* kp = (const uint4*)(kb + r16 * HD + grp * DL);
     const uint4* vp = (const uint4*)(vb + grp * HD * 4 + r16 * NO * 4);
 #pragma unroll
     for (int c = 0; c < NQ; ++c) kreg[c] = kp[c];
 #pragma unroll
     for (int c = 0; c < NV; ++c) vreg[c] = vp[c];
+  };
+
+  uint4 kcur[NQ], vcur[NV];
+  const int stride = W * G;
+  int p = g * W + wave;
+  if (p < n_pages) load_page(p, kcur, vcur);
+  __syncthreads();  // q tile ready
+  for (; p < n_pages; p += stride) {
+    uint4 knext[NQ], vnext[NV];
+    if (p + stride < n_pages) load_page(p + stride, knext, vnext);
 
     f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
+    asm volatile("" ::: "memory");  // re-read the q tile from LDS each page (keeps it out of registers)
 #pragma unroll
     for (int c = 0; c < NQ; ++c) {
-      if constexpr (sizeof(T) == 2) {
-        S = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kreg[c]),
-                                                   __builtin_bit_cast(f16x8, qreg[c]), S, 0, 0, 0);
+      const uint4 qv = sm_q[lane * NQ + c];
+      if constexpr (sizeof(TK) == 2) {
+        S = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kcur[c]),
+                                                   __builtin_bit_cast(f16x8, qv), S, 0, 0, 0);
       } else {
-        S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kreg[c].x), __uint_as_float(qreg[c].x), S, 0, 0, 0);
-        S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kreg[c].y), __uint_as_float(qreg[c].y), S, 0, 0, 0);
-        S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kreg[c].z), __uint_as_float(qreg[c].z), S, 0, 0, 0);
-        S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kreg[c].w), __uint_as_float(qreg[c].w), S, 0, 0, 0);
+        S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kcur[c].x), __uint_as_float(qv.x), S, 0, 0, 0);
+        S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kcur[c].y), __uint_as_float(qv.y), S, 0, 0, 0);
+        S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kcur[c].z), __uint_as_float(qv.z), S, 0, 0, 0);
+        S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kcur[c].w), __uint_as_float(qv.w), S, 0, 0, 0);
       }
     }
 
@@ -145,77 +164,130 @@ __global__ __launch_bounds__(64) void k_attn(AttnArgs a) {
       for (int n = 0; n < NO; ++n) O[n][v] *= av;
     }
 
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (sizeof(TK) == 2) {
       // A = P[node r16][tokens 4*grp..+3]; B = V[tokens 4*grp..+3][dim NO*r16 + n]
       const unsigned p01 = pack_f16x2(pv[0], pv[1]), p23 = pack_f16x2(pv[2], pv[3]);
       const f16x4 A = __builtin_bit_cast(f16x4, uint2{p01, p23});
-      const uint2* v2 = (const uint2*)vreg;
+      const uint2* v2 = (const uint2*)vcur;
 #pragma unroll
       for (int n = 0; n < NO; ++n)
         O[n] = __builtin_amdgcn_mfma_f32_16x16x16f16(A, __builtin_bit_cast(f16x4, v2[n]), O[n], 0, 0, 0);
     } else {
-      const float* vf = (const float*)vreg;
+      const float* vf = (const float*)vcur;
 #pragma unroll
       for (int v = 0; v < 4; ++v)
 #pragma unroll
         for (int n = 0; n < NO; ++n)
           O[n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[v], vf[n * 4 + v], O[n], 0, 0, 0);
     }
+#pragma unroll
+    for (int c = 0; c < NQ; ++c) kcur[c] = knext[c];
+#pragma unroll
+    for (int c = 0; c < NV; ++c) vcur[c] = vnext[c];
   }
 
-  const size_t pbase = ((size_t)head * a.nsplit + split) * a.Mp;
-  if (grp == 0 && qn < M) {
-    a.part_ml[(pbase + qn) * 2 + 0] = m_run;
-    a.part_ml[(pbase + qn) * 2 + 1] = l_run;
+  // Merge the waves' states: O = sum_w f_w O_w / sum_w f_w l_w with
+  // f_w = 2^(m_w - max_w m_w), summed in wave order.
+  constexpr int OS = NO * 4 + 1;
+  float* sm_m = smem + 64 * NQ * 4;       // [W][16], after the q tile
+  float* sm_l = sm_m + W * 16;            // [W][16]
+  float* sm_o = sm_l + W * 16;            // [W][64][OS]
+  if (grp == 0) {
+    sm_m[wave * 16 + r16] = m_run;
+    sm_l[wave * 16 + r16] = l_run;
   }
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int node = qt * 16 + grp * 4 + v;
-    if (node < M) {
-      float* dst = a.part_o + (pbase + node) * HD + NO * r16;
+  for (int n = 0; n < NO; ++n)
 #pragma unroll
-      for (int n = 0; n < NO; ++n) dst[n] = O[n][v];
+    for (int v = 0; v < 4; ++v) sm_o[(wave * 64 + lane) * OS + n * 4 + v] = O[n][v];
+  __syncthreads();
+
+  // Workgroup state: per row (m, l) and per output position the unnormalised
+  // sum.  Output position e = (source lane, n, v): node row 4*(lane/16)+v,
+  // dim NO*(lane%16)+n.
+  const size_t tile = (size_t)head * gridDim.y + qt;       // (head, node tile)
+  float* pm = a.part_ml + (tile * G + g) * 32;             // [16][2]
+  float* po = a.part_o + (tile * G + g) * 16 * HD;         // [16][HD]
+  for (int e = threadIdx.x; e < 64 * NO * 4; e += blockDim.x) {
+    const int src = e / (NO * 4), n = (e / 4) % NO, v = e % 4;
+    const int row = (src >> 4) * 4 + v;
+    const int node = qt * 16 + row;
+    if (node >= M) continue;
+    float mx = -1e30f;
+    for (int w = 0; w < W; ++w) mx = fmaxf(mx, sm_m[w * 16 + row]);
+    float num = 0.f, den = 0.f;
+    for (int w = 0; w < W; ++w) {
+      const float f = exp2f(sm_m[w * 16 + row] - mx);
+      den += f * sm_l[w * 16 + row];
+      num += f * sm_o[(w * 64 + src) * OS + n * 4 + v];
+    }
+    const int dim = NO * (src & 15) + n;
+    if (G == 1) {
+      store_act<TW>(a.o, a.o_plane, (size_t)node * a.d + head * HD + dim, num / den);
+    } else {
+      po[row * HD + dim] = num;
+      if ((src & 15) == 0 && n == 0) {  // one writer per row: source lane 16 * (row / 4), n = 0
+        pm[row * 2 + 0] = mx;
+        pm[row * 2 + 1] = den;
+      }
     }
   }
-}
+  if (G == 1) return;
 
-// T = weight type of the mode (selects the activation plane format of o).
-template <typename T, int HD>
-__global__ __launch_bounds__(HD) void k_combine(CombineArgs a) {
-  const int head = blockIdx.x, node = blockIdx.y, dim = threadIdx.x;
-  const size_t base = (size_t)head * a.nsplit * a.Mp;
-  float mx = -1e30f;
-  for (int s = 0; s < a.nsplit; ++s) mx = fmaxf(mx, a.part_ml[(base + (size_t)s * a.Mp + node) * 2]);
-  float num = 0.f, den = 0.f;
-  for (int s = 0; s < a.nsplit; ++s) {
-    const size_t r = base + (size_t)s * a.Mp + node;
-    const float w = exp2f(a.part_ml[r * 2] - mx);
-    den += w * a.part_ml[r * 2 + 1];
-    num += w * a.part_o[r * HD + dim];
+  // Publish this workgroup's partial, then let the last arrival merge.  The
+  // barrier completes every wave's stores; one thread's device-scope fence
+  // then releases them (and, in the last workgroup, acquires the others'):
+  // on this multi-XCD part a fence writes back / invalidates L2, so it is
+  // issued once per workgroup, not per thread.
+  __shared__ int last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    const int prev = atomicAdd(a.counters + tile, 1);
+    last = prev == G - 1;
+    if (last) __threadfence();
   }
-  store_act<T>(a.o, a.o_plane, (size_t)node * a.d + head * HD + dim, num / den);
+  __syncthreads();
+  if (!last) return;
+  const float* pm0 = a.part_ml + tile * G * 32;
+  const float* po0 = a.part_o + tile * G * 16 * HD;
+  for (int e = threadIdx.x; e < 16 * HD; e += blockDim.x) {
+    const int row = e / HD, dim = e % HD;
+    const int node = qt * 16 + row;
+    if (node >= M) continue;
+    float mx = -1e30f;
+    for (int k = 0; k < G; ++k) mx = fmaxf(mx, pm0[k * 32 + row * 2]);
+    float num = 0.f, den = 0.f;
+    for (int k = 0; k < G; ++k) {
+      const float f = exp2f(pm0[k * 32 + row * 2] - mx);
+      den += f * pm0[k * 32 + row * 2 + 1];
+      num += f * po0[(size_t)k * 16 * HD + row * HD + dim];
+    }
+    store_act<TW>(a.o, a.o_plane, (size_t)node * a.d + head * HD + dim, num / den);
+  }
+  if (threadIdx.x == 0) a.counters[tile] = 0;
 }
 
-template <typename T, int HD>
+template <typename TK, typename TW, int HD>
 static hipError_t attn_t(int qt, const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((k_attn<T, HD>), dim3(a.nsplit, a.n_heads, qt), dim3(64), 0, s, a);
+  constexpr int NO = HD / 16;
+  constexpr int NQ = HD / 4 * (int)sizeof(TK) / 16;
+  const size_t lds = (size_t)(64 * NQ * 4 + kAttnWaves * 16 * 2 + kAttnWaves * 64 * (NO * 4 + 1)) * 4;
+  static bool attr = false;
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute((const void*)k_attn<TK, TW, HD>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  hipLaunchKernelGGL((k_attn<TK, TW, HD>), dim3(a.n_heads, qt, a.groups), dim3(kAttnWaves * 64), lds, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_attn(bool bf16, int head_dim, int qt, const AttnArgs& a, hipStream_t s) {
-  if (bf16) return head_dim == 128 ? attn_t<_Float16, 128>(qt, a, s) : attn_t<_Float16, 64>(qt, a, s);
-  return head_dim == 128 ? attn_t<float, 128>(qt, a, s) : attn_t<float, 64>(qt, a, s);
-}
-
-template <typename T, int HD>
-static hipError_t combine_t(const CombineArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((k_combine<T, HD>), dim3(a.n_heads, a.M), dim3(HD), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_combine(bool bf16, int head_dim, const CombineArgs& a, hipStream_t s) {
-  if (bf16) return head_dim == 128 ? combine_t<__bf16, 128>(a, s) : combine_t<__bf16, 64>(a, s);
-  return head_dim == 128 ? combine_t<float, 128>(a, s) : combine_t<float, 64>(a, s);
+  if (bf16)
+    return head_dim == 128 ? attn_t<_Float16, __bf16, 128>(qt, a, s) : attn_t<_Float16, __bf16, 64>(qt, a, s);
+  return head_dim == 128 ? attn_t<float, float, 128>(qt, a, s) : attn_t<float, float, 64>(qt, a, s);
 }
 
 }  // namespace tss

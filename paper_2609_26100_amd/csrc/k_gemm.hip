@@ -53,14 +53,22 @@ __device__ __forceinline__ f32x4 mfma_chunk<float>(const uint4& a, const uint4& 
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-// Chunk loads in flight per wave (register budget of a 1024-thread
-// workgroup: 128 VGPRs per lane).
+// Weight tiles are read exactly once per step: nontemporal loads keep them
+// from displacing the activations that every workgroup re-reads from L2.
+__device__ __forceinline__ uint4 load_stream(const uint8_t* p) {
+  typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+  const u4v v = __builtin_nontemporal_load((const u4v*)p);
+  return uint4{v.x, v.y, v.z, v.w};
+}
+
+// Chunk loads in flight per wave (register budget of a 512-thread
+// workgroup: 256 VGPRs per lane, kept well below for occupancy).
 template <int MT, int NT> struct Cpw {
   static constexpr int v = (MT == 1 && NT == 1) ? 8 : ((MT * NT) <= 2 ? 4 : ((MT * NT) <= 4 ? 2 : 1));
 };
 
 template <typename T, int MT, int NT, int EPI>
-__global__ __launch_bounds__(1024) void k_gemm(GemmArgs a) {
+__global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
   constexpr int KL = KC / 4;           // K elements per lane per tile
   constexpr int CPW = Cpw<MT, NT>::v;
@@ -84,6 +92,17 @@ __global__ __launch_bounds__(1024) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // The RMSNorm partial sums of this wave's row are loaded before the weight
+  // stream (when every row has its own wave), so their latency hides behind it.
+  constexpr int SSV = 8;  // parts per lane: up to 512 parts per row
+  const bool ss_early = a.ss_in && M <= waves;
+  float ssv[SSV];
+#pragma unroll
+  for (int i = 0; i < SSV; ++i) {
+    const int p = lane + 64 * i;
+    ssv[i] = (ss_early && wave < M && p < a.ss_nparts) ? a.ss_in[(size_t)wave * a.ss_stride + p] : 0.f;
+  }
+
   for (int base = wave * CPW; base < nkc; base += waves * CPW) {
     uint4 wv[CPW][NT];
     uint4 xv[CPW][MT][S];
@@ -93,7 +112,7 @@ __global__ __launch_bounds__(1024) void k_gemm(GemmArgs a) {
       const bool in = c < nkc;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        wv[i][nt] = in ? *(const uint4*)(wstrip + ((size_t)c * NT + nt) * kTileBytes) : uint4{0, 0, 0, 0};
+        wv[i][nt] = in ? load_stream(wstrip + ((size_t)c * NT + nt) * kTileBytes) : uint4{0, 0, 0, 0};
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = mt * 16 + r16;
@@ -130,10 +149,23 @@ __global__ __launch_bounds__(1024) void k_gemm(GemmArgs a) {
 
   // RMSNorm row scale from the producer's partial sums (fixed order, so every
   // workgroup derives the same value).
-  if (a.ss_in) {
+  if (ss_early) {
+    if (wave < M) {
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < SSV; ++i) s += ssv[i];
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+      if (lane == 0) rscale[wave] = rsqrtf(s / (float)a.norm_dim + a.eps);
+    }
+  } else if (a.ss_in) {
     for (int m = wave; m < M; m += waves) {
       float s = 0.f;
-      for (int p = lane; p < a.ss_nparts; p += 64) s += a.ss_in[(size_t)p * a.Mp + m];
+#pragma unroll
+      for (int i = 0; i < SSV; ++i) {
+        const int p = lane + 64 * i;
+        s += p < a.ss_nparts ? a.ss_in[(size_t)m * a.ss_stride + p] : 0.f;
+      }
 #pragma unroll
       for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
       if (lane == 0) rscale[m] = rsqrtf(s / (float)a.norm_dim + a.eps);
@@ -197,7 +229,7 @@ __global__ __launch_bounds__(1024) void k_gemm(GemmArgs a) {
     for (int row = threadIdx.x; row < M; row += blockDim.x) {
       float s = 0.f;
       for (int col = 0; col < COLS; ++col) s += aux[row * COLS + col];
-      a.ss_out[(size_t)strip * a.Mp + row] = s;
+      a.ss_out[(size_t)row * a.ss_stride + strip] = s;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
     static_assert(NT == 2, "gate and up tiles pair up in one strip");
@@ -221,8 +253,8 @@ __global__ __launch_bounds__(1024) void k_gemm(GemmArgs a) {
         const float v = yfin[row * COLS + col];
         if (v > bv) { bv = v; bi = col; }
       }
-      a.am_val[(size_t)strip * a.Mp + row] = bv;
-      a.am_idx[(size_t)strip * a.Mp + row] = n0 + bi;
+      a.am_val[(size_t)row * a.am_stride + strip] = bv;
+      a.am_idx[(size_t)row * a.am_stride + strip] = n0 + bi;
     }
   }
 }
@@ -232,9 +264,10 @@ static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
   const int nt = strip_tiles(epi);
   const int strips = a.N / (16 * nt);
   const int cpw = nt == 2 ? Cpw<MT, 2>::v : Cpw<MT, 1>::v;
-  // enough waves to cover K with CPW-chunk blocks, capped by LDS (64 KiB) and 16
+  // enough waves to cover K with CPW-chunk blocks, capped by LDS (64 KiB) and 8
+  // (8-wave workgroups measured best across the 7B shapes)
   int waves = (a.nkc + cpw - 1) / cpw;
-  if (waves > 16) waves = 16;
+  if (waves > 8) waves = 8;
   const int rows = MT * 16, cols = nt * 16;
   while (waves > 1 && (size_t)(waves * rows * cols + rows * cols * 2 + rows) * 4 > 65536) waves >>= 1;
   const size_t lds = (size_t)(waves * rows * cols + rows * cols * 2 + rows) * 4;

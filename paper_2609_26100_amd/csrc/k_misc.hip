@@ -7,19 +7,43 @@ namespace tss {
 
 // h[m] = E[tok[m]] (fp32); xn[m] = h[m] * gain (activation planes) for the
 // first RMSNorm the rows meet; ss_out[m] = sum h[m]^2 (one partial,
-// fixed-order reduction).
+// fixed-order reduction).  Each thread gathers up to four 16-byte chunks of
+// the row, issued together.  The step's parameters arrive by value and
+// workgroup 0 stores them for the later kernels of the step (this replaces a
+// separate host-to-device copy, which costs as much as a kernel launch).
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
+  constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte chunk
+  constexpr int MAXC = 4;                 // chunks per thread (d <= 4 * 256 * E)
   __shared__ float red[256];
   const int m = blockIdx.x;
-  const int d = a.d;
-  const T* row = (const T*)a.embed + (size_t)a.sp->tok[m] * d;
+  const int d = a.d, nch = d / E;
+  if (m == 0) {
+    const uint32_t* src = (const uint32_t*)&a.sp;
+    uint32_t* dst = (uint32_t*)a.sp_dev;
+    for (int i = threadIdx.x; i < (int)(sizeof(StepParams) / 4); i += 256) dst[i] = src[i];
+  }
+  const T* row = (const T*)a.embed + (size_t)a.sp.tok[m] * d;
+  uint4 raw[MAXC];
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = threadIdx.x + i * 256;
+    raw[i] = c < nch ? ((const uint4*)row)[c] : uint4{0, 0, 0, 0};
+  }
   float s = 0.f;
-  for (int k = threadIdx.x; k < d; k += 256) {
-    const float v = (float)row[k];
-    a.h[(size_t)m * d + k] = v;
-    store_act<T>(a.xn, a.xn_plane, (size_t)m * d + k, v * a.gain[k]);
-    s += v * v;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = threadIdx.x + i * 256;
+    if (c >= nch) break;
+    const T* e = (const T*)&raw[i];
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int k = c * E + j;
+      const float v = (float)e[j];
+      a.h[(size_t)m * d + k] = v;
+      store_act<T>(a.xn, a.xn_plane, (size_t)m * d + k, v * a.gain[k]);
+      s += v * v;
+    }
   }
   red[threadIdx.x] = s;
   __syncthreads();
@@ -27,7 +51,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
     __syncthreads();
   }
-  if (threadIdx.x == 0) a.ss_out[m] = red[0];
+  if (threadIdx.x == 0) a.ss_out[(size_t)m * a.ss_stride] = red[0];
 }
 
 // (value, index) order of the greedy argmax: larger value first, lower index on ties.
@@ -35,20 +59,46 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
-// One workgroup.  Greedy token per node from the lm_head's per-strip partials,
-// then the accept scan over the tree: a node is accepted when its parent is
-// and its token equals the parent's greedy token; the deepest accepted node
-// (lowest id among equal depths) gives accept_len and the bonus token.
-__global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
+// One workgroup of 16 waves.  Greedy token per node from the lm_head's
+// per-strip partials (each node gets 16 / M waves, loads issued eight at a
+// time), then the accept scan over the tree: a node is accepted when its
+// parent is and its token equals the parent's greedy token; the deepest
+// accepted node (lowest id among equal depths) gives accept_len and the bonus
+// token.
+__global__ __launch_bounds__(1024) void k_accept(AcceptArgs a) {
   __shared__ int32_t g[kMaxNodes];
+  __shared__ float bvs[16];
+  __shared__ int32_t bis[16];
+  __shared__ int32_t s_tok[kMaxNodes], s_par[kMaxNodes], s_dep[kMaxNodes];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int m = wave; m < a.M; m += 4) {
+  const int M = a.M;
+  if (threadIdx.x < M) {
+    s_tok[threadIdx.x] = a.sp->tok[threadIdx.x];
+    s_par[threadIdx.x] = a.sp->parent[threadIdx.x];
+    s_dep[threadIdx.x] = a.sp->depth[threadIdx.x];
+  }
+  const int wpr = M >= 16 ? 1 : (M >= 8 ? 2 : (M >= 4 ? 4 : (M >= 2 ? 8 : 16)));  // waves per node
+  const int groups = 16 / wpr;
+  const int grp_id = wave / wpr, sub = wave % wpr;
+  for (int m0 = 0; m0 < M; m0 += groups) {
+    const int m = m0 + grp_id;
     float bv = -INFINITY;
     int bi = 0x7fffffff;
-    for (int p = lane; p < a.nparts; p += 64) {
-      const float v = a.am_val[(size_t)p * a.Mp + m];
-      const int i = a.am_idx[(size_t)p * a.Mp + m];
-      if (better(v, i, bv, bi)) { bv = v; bi = i; }
+    if (m < M) {
+      const int stride = 64 * wpr;
+      for (int p = sub * 64 + lane; p < a.nparts; p += 8 * stride) {
+        float v[8];
+        int ix[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int q = p + u * stride;
+          v[u] = q < a.nparts ? a.am_val[(size_t)m * a.am_stride + q] : -INFINITY;
+          ix[u] = q < a.nparts ? a.am_idx[(size_t)m * a.am_stride + q] : 0x7fffffff;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (better(v[u], ix[u], bv, bi)) { bv = v[u]; bi = ix[u]; }
+      }
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
@@ -57,31 +107,39 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
     }
     if (lane == 0) {
+      bvs[wave] = bv;
+      bis[wave] = bi;
+    }
+    __syncthreads();
+    if (sub == 0 && lane == 0 && m < M) {
+      for (int w = 1; w < wpr; ++w)
+        if (better(bvs[wave + w], bis[wave + w], bv, bi)) { bv = bvs[wave + w]; bi = bis[wave + w]; }
       g[m] = bi;
       a.greedy[m] = bi;
     }
+    __syncthreads();
   }
-  __syncthreads();
   if (threadIdx.x == 0) {
-    const StepParams* sp = a.sp;
     uint64_t acc = 1ull;  // bit i: node i accepted
     int best = 0;
-    for (int i = 1; i < a.M; ++i) {
-      const int p = sp->parent[i];
-      if (((acc >> p) & 1ull) && sp->tok[i] == g[p]) {
+    for (int i = 1; i < M; ++i) {
+      const int p = s_par[i];
+      if (((acc >> p) & 1ull) && s_tok[i] == g[p]) {
         acc |= 1ull << i;
-        if (sp->depth[i] > sp->depth[best]) best = i;
+        if (s_dep[i] > s_dep[best]) best = i;
       }
     }
-    Result* r = a.result;
-    const int len = sp->depth[best];
-    r->accept_len = len;
-    r->next_token = g[best];
-    r->best = best;
-    r->path_len = len + 1;
-    for (int j = best, dd = len; dd >= 0; --dd) {
-      r->path[dd] = j;
-      j = dd > 0 ? sp->parent[j] : 0;
+    const int len = s_dep[best];
+    for (int copy = 0; copy < 2; ++copy) {
+      Result* r = copy == 0 ? a.result : a.result_host;
+      r->accept_len = len;
+      r->next_token = g[best];
+      r->best = best;
+      r->path_len = len + 1;
+      for (int j = best, dd = len; dd >= 0; --dd) {
+        r->path[dd] = j;
+        j = dd > 0 ? s_par[j] : 0;
+      }
     }
   }
 }
@@ -140,7 +198,7 @@ hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_accept, dim3(1), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_accept, dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 

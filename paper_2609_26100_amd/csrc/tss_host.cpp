@@ -22,7 +22,7 @@ using namespace tss;
 
 namespace {
 
-constexpr int kMaxSplit = 64;
+constexpr size_t kStageBytes = 32u << 20;  // one pinned weight-upload buffer
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -36,7 +36,8 @@ struct WeightLayout {
 };
 
 struct WsLayout {
-  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, logits, am_val, am_idx, greedy, total;
+  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, counters, logits, am_val, am_idx, greedy,
+      total;
 };
 
 // weight element bytes; the KV cache uses the same width (fp16 in the bf16
@@ -52,6 +53,7 @@ int cfg_ok(const tss_model_cfg* c) {
   if (c->head_dim != 64 && c->head_dim != 128) return 0;
   if (c->n_heads < 1 || c->d_model != c->n_heads * c->head_dim) return 0;
   if (c->d_model % 32 || c->ffn_dim < 32 || c->ffn_dim % 32 || c->vocab < 32 || c->vocab % 32) return 0;
+  if (c->d_model > 8192) return 0;  // RMSNorm partial sums: at most 512 per row
   if (c->dtype != TSS_F32 && c->dtype != TSS_BF16) return 0;
   if (c->max_nodes < 1 || c->max_nodes > kMaxNodes) return 0;
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return 0;
@@ -96,8 +98,10 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   w.q = take(Mp * d * 4);
   w.o = take(ap * Mp * d * es);
   w.act = take(ap * Mp * f * es);
-  w.part_o = take((size_t)c->n_heads * kMaxSplit * Mp * c->head_dim * 4);
-  w.part_ml = take((size_t)c->n_heads * kMaxSplit * Mp * 2 * 4);
+  const size_t tiles = (size_t)c->n_heads * (Mp / 16);
+  w.part_o = take(tiles * kAttnMaxGroups * 16 * c->head_dim * 4);
+  w.part_ml = take(tiles * kAttnMaxGroups * 16 * 2 * 4);
+  w.counters = take(tiles * 4);
   w.logits = take(Mp * v * 4);
   w.am_val = take((v / 16) * Mp * 4);
   w.am_idx = take((v / 16) * Mp * 4);
@@ -142,9 +146,14 @@ struct tss_ctx {
   std::vector<int32_t> n_kv;
   std::vector<std::vector<int32_t>> kv_len;
   std::vector<std::vector<uint8_t>> mask;
-  // pinned host staging
+  // pinned host staging: step parameters and result, and two weight-upload
+  // buffers (packing one while the other is copied)
+  uint8_t* stage[2] = {nullptr, nullptr};
+  hipEvent_t stage_ev[2] = {nullptr, nullptr};
+  int stage_cur = 0;
   StepParams* sp_host = nullptr;
-  Result* res_host = nullptr;
+  Result* res_host = nullptr;     // host-mapped, written by the accept kernel
+  Result* res_dev_map = nullptr;  // its device address
   int last_M = 0;
   bool poisoned = false;
   std::string err;
@@ -308,7 +317,12 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
   c->wl = weight_layout(cfg);
   c->wsl = ws_layout(cfg);
   hipError_t e = hipHostMalloc((void**)&c->sp_host, sizeof(StepParams), hipHostMallocDefault);
-  if (e == hipSuccess) e = hipHostMalloc((void**)&c->res_host, sizeof(Result), hipHostMallocDefault);
+  if (e == hipSuccess)
+    e = hipHostMalloc((void**)&c->res_host, sizeof(Result), hipHostMallocMapped | hipHostMallocCoherent);
+  if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&c->res_dev_map, c->res_host, 0);
+  if (e == hipSuccess) e = hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * (c->Mp / 16) * 4,
+                                          c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
   if (e == hipSuccess) e = hipEventCreate(&c->ev0);
   if (e == hipSuccess) e = hipEventCreate(&c->ev1);
   if (e != hipSuccess) {
@@ -321,6 +335,13 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
 
 void tss_destroy(tss_ctx* c) {
   if (!c) return;
+  for (int i = 0; i < 2; ++i) {
+    if (c->stage_ev[i]) {
+      (void)hipEventSynchronize(c->stage_ev[i]);
+      (void)hipEventDestroy(c->stage_ev[i]);
+    }
+    if (c->stage[i]) (void)hipHostFree(c->stage[i]);
+  }
   if (c->sp_host) (void)hipHostFree(c->sp_host);
   if (c->res_host) (void)hipHostFree(c->res_host);
   if (c->ev0) (void)hipEventDestroy(c->ev0);
@@ -338,9 +359,34 @@ int tss_load_weights(tss_ctx* c, int32_t first, int32_t count, const void* const
   for (int i = 0; i < count; ++i)
     if (!host_tensors[i]) return fail(c, TSS_EINVAL, "null tensor pointer");
   HIPCHK(hipStreamSynchronize(c->stream), "sync before weight load");
-  std::vector<uint8_t> buf;
-  auto h2d = [&](size_t off, const void* src, size_t bytes) {
-    return hipMemcpy(c->w + off, src, bytes, hipMemcpyHostToDevice);
+  if (!c->stage[0]) {
+    for (int i = 0; i < 2; ++i) {
+      HIPCHK(hipHostMalloc((void**)&c->stage[i], kStageBytes, hipHostMallocDefault), "pinned staging");
+      HIPCHK(hipEventCreateWithFlags(&c->stage_ev[i], hipEventDisableTiming), "staging event");
+      HIPCHK(hipEventRecord(c->stage_ev[i], c->stream), "staging event");
+    }
+  }
+  // Takes the next staging buffer once its previous copy has drained.
+  auto next_stage = [&](uint8_t** buf) -> hipError_t {
+    const int i = c->stage_cur;
+    c->stage_cur ^= 1;
+    *buf = c->stage[i];
+    return hipEventSynchronize(c->stage_ev[i]);
+  };
+  auto stage_done = [&](int used) { return hipEventRecord(c->stage_ev[used], c->stream); };
+  auto raw = [&](size_t off, const void* src, size_t bytes) -> hipError_t {
+    for (size_t done = 0; done < bytes; done += kStageBytes) {
+      const size_t n = std::min(kStageBytes, bytes - done);
+      const int used = c->stage_cur;
+      uint8_t* b;
+      hipError_t e = next_stage(&b);
+      if (e != hipSuccess) return e;
+      std::memcpy(b, (const uint8_t*)src + done, n);
+      e = hipMemcpyAsync(c->w + off + done, b, n, hipMemcpyHostToDevice, c->stream);
+      if (e == hipSuccess) e = stage_done(used);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
   };
   auto gain = [&](size_t off, const void* src) {
     std::vector<float> g(d);
@@ -353,52 +399,64 @@ int tss_load_weights(tss_ctx* c, int32_t first, int32_t count, const void* const
     } else {
       std::memcpy(g.data(), src, (size_t)d * 4);
     }
-    return h2d(off, g.data(), (size_t)d * 4);
+    return raw(off, g.data(), (size_t)d * 4);
   };
-  auto plain = [&](size_t off, const void* src, int rows, int K) {
-    buf.resize((size_t)rows * K * es);
-    pack_tiles(buf.data(), (const uint8_t*)src, rows, K, es, kTileBytes, [](int n) { return n; });
-    return h2d(off, buf.data(), buf.size());
+  // Packs src [rows][K] in batches of row tiles through the staging buffers.
+  // slot < 0: single-tile strips (tile (r, c) at (r * nkc + c) KiB); slot 0/1:
+  // gate/up pairs (tile (r, c) at ((r * nkc + c) * 2 + slot) KiB).
+  auto packed = [&](size_t off, const void* src, int rows, int K, int slot, auto row_map) -> hipError_t {
+    const int nkc = K / c->KC;
+    const size_t rt_bytes = (size_t)nkc * kTileBytes;
+    const int per_batch = (int)std::max<size_t>(1, kStageBytes / rt_bytes);
+    const int rts = rows / 16;
+    for (int r0 = 0; r0 < rts; r0 += per_batch) {
+      const int r1 = std::min(rts, r0 + per_batch);
+      const int used = c->stage_cur;
+      uint8_t* b;
+      hipError_t e = next_stage(&b);
+      if (e != hipSuccess) return e;
+      pack_tiles(b, (const uint8_t*)src, (r1 - r0) * 16, K, es, kTileBytes,
+                 [&](int n) { return row_map(r0 * 16 + n); });
+      if (slot < 0)
+        e = hipMemcpyAsync(c->w + off + (size_t)r0 * rt_bytes, b, (size_t)(r1 - r0) * rt_bytes, hipMemcpyHostToDevice,
+                           c->stream);
+      else
+        e = hipMemcpy2DAsync(c->w + off + ((size_t)r0 * nkc * 2 + slot) * kTileBytes, 2 * kTileBytes, b, kTileBytes,
+                             kTileBytes, (size_t)(r1 - r0) * nkc, hipMemcpyHostToDevice, c->stream);
+      if (e == hipSuccess) e = stage_done(used);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
   };
+  auto ident = [](int n) { return n; };
   for (int i = 0; i < count; ++i) {
     const int t = first + i;
     const void* src = host_tensors[i];
     hipError_t e = hipSuccess;
     if (t == 0) {
-      e = h2d(c->wl.embed, src, (size_t)v * d * es);
+      e = raw(c->wl.embed, src, (size_t)v * d * es);
     } else if (t == 1 + 9 * L) {
       e = gain(c->wl.final_norm, src);
     } else if (t == 2 + 9 * L) {
-      e = plain(c->wl.lm_head, src, v, d);
+      e = packed(c->wl.lm_head, src, v, d, -1, ident);
     } else {
       const int l = (t - 1) / 9, j = (t - 1) % 9;
       const LayerW& W = c->wl.layers[l];
+      const int hd = c->cfg.head_dim;
       switch (j) {
         case 0: e = gain(W.attn_norm, src); break;
-        case 1: case 2: case 3: {
-          const int hd = c->cfg.head_dim;
-          buf.resize((size_t)d * d * es);
-          pack_tiles(buf.data(), (const uint8_t*)src, d, d, es, kTileBytes,
-                     [hd](int n) { return qkv_src_row(n, hd); });
-          e = h2d(W.qkv + (size_t)(j - 1) * d * d * es, buf.data(), buf.size());
+        case 1: case 2: case 3:
+          e = packed(W.qkv + (size_t)(j - 1) * d * d * es, src, d, d, -1, [hd](int n) { return qkv_src_row(n, hd); });
           break;
-        }
-        case 4: e = plain(W.o, src, d, d); break;
+        case 4: e = packed(W.o, src, d, d, -1, ident); break;
         case 5: e = gain(W.mlp_norm, src); break;
-        case 6: case 7: {
-          // gate tile s and up tile s share strip s: 2 KiB per K chunk, gate first
-          buf.resize((size_t)f * d * es);
-          pack_tiles(buf.data(), (const uint8_t*)src, f, d, es, kTileBytes, [](int n) { return n; });
-          const size_t n_tiles = (size_t)(f / 16) * (d / c->KC);
-          e = hipMemcpy2D(c->w + W.gateup + (j - 6) * kTileBytes, 2 * kTileBytes, buf.data(), kTileBytes, kTileBytes,
-                          n_tiles, hipMemcpyHostToDevice);
-          break;
-        }
-        default: e = plain(W.down, src, d, f); break;
+        case 6: case 7: e = packed(W.gateup, src, f, d, j - 6, ident); break;
+        default: e = packed(W.down, src, d, f, -1, ident); break;
       }
     }
     if (e != hipSuccess) return hip_fail(c, e, "weight upload");
   }
+  HIPCHK(hipStreamSynchronize(c->stream), "weight upload");
   return TSS_OK;
 }
 
@@ -524,20 +582,20 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
   };
 
   c->prof_armed = false;
-  HIPCHK(hipMemcpyAsync(sp_dev, c->sp_host, sizeof(StepParams), hipMemcpyHostToDevice, s), "step params");
 
   {
     EmbedArgs a{};
     a.embed = c->w + c->wl.embed;
-    a.sp = sp_dev;
+    a.sp = sp;
+    a.sp_dev = sp_dev;
     a.gain = attn_gain(0);
     a.h = (float*)(ws + c->wsl.h);
     a.xn = ws + c->wsl.xa;
     a.xn_plane = act_planes(&cf) == 2 ? (size_t)c->Mp * d : 0;
     a.ss_out = (float*)(ws + c->wsl.ss_a);
+    a.ss_stride = d / 16;
     a.d = d;
     a.M = M;
-    a.Mp = c->Mp;
     ProfScope ps(c, TSS_K_EMBED, -1);
     HIPCHK(launch_embed(c->bf16, a, s), "embed");
     ps.done();
@@ -550,15 +608,14 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
   const size_t plane_d = two ? (size_t)c->Mp * d : 0, plane_f = two ? (size_t)c->Mp * f : 0;
   base.eps = cf.rms_eps;
   base.norm_dim = d;
+  base.ss_stride = d / 16;
+  base.am_stride = cf.vocab / 16;
   base.sp = sp_dev;
 
-  // attention split: about 1024 waves over (split, head, node tile)
-  const int total = sp.n_kv + M;
-  const int n_pages = (total + kPage - 1) / kPage;
-  const int target = std::max(1, 1024 / (H * mt));
-  int pps = std::max(1, (n_pages + target - 1) / target);
-  while ((n_pages + pps - 1) / pps > kMaxSplit) ++pps;
-  const int nsplit = (n_pages + pps - 1) / pps;
+  // attention: one page per wave where possible, at most kAttnMaxGroups
+  // sixteen-wave workgroups per (head, node tile)
+  const int n_pages = (sp.n_kv + M + kPage - 1) / kPage;
+  const int attn_groups = std::max(1, std::min(kAttnMaxGroups, (n_pages + 15) / 16));
 
   for (size_t idx = 0; idx < active.size(); ++idx) {
     const int l = active[idx];
@@ -586,37 +643,27 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
       HIPCHK(launch_gemm(c->bf16, EPI_QKV, mt, a, s), "qkv gemm");
       ps.done();
     }
-    {  // tree attention + split combine
+    {  // tree attention
       AttnArgs a{};
       a.q = (const float*)(ws + c->wsl.q);
       a.kv_pages = pages;
       a.page_table = pt;
       a.sp = sp_dev;
+      a.o = ws + c->wsl.o;
+      a.o_plane = plane_d;
       a.part_o = (float*)(ws + c->wsl.part_o);
       a.part_ml = (float*)(ws + c->wsl.part_ml);
+      a.counters = (int*)(ws + c->wsl.counters);
+      a.groups = attn_groups;
       a.layer = l;
       a.n_pages_pool = c->kvl.n_pages;
       a.n_heads = H;
       a.d = d;
       a.M = M;
-      a.Mp = c->Mp;
       a.n_kv = sp.n_kv;
-      a.pages_per_split = pps;
-      a.nsplit = nsplit;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
       ProfScope ps(c, TSS_K_ATTN, l);
       HIPCHK(launch_attn(c->bf16, hd, mt, a, s), "attention");
-      CombineArgs cb{};
-      cb.part_o = a.part_o;
-      cb.part_ml = a.part_ml;
-      cb.o = ws + c->wsl.o;
-      cb.o_plane = plane_d;
-      cb.n_heads = H;
-      cb.d = d;
-      cb.M = M;
-      cb.Mp = c->Mp;
-      cb.nsplit = nsplit;
-      HIPCHK(launch_combine(c->bf16, hd, cb, s), "attention combine");
       ps.done();
     }
     {  // O projection + residual; next norm input
@@ -695,10 +742,11 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
       a.am_idx = (const int32_t*)(ws + c->wsl.am_idx);
       a.nparts = cf.vocab / 16;
       a.M = M;
-      a.Mp = c->Mp;
+      a.am_stride = cf.vocab / 16;
       a.sp = sp_dev;
       a.greedy = (int32_t*)(ws + c->wsl.greedy);
       a.result = (Result*)(ws + c->wsl.result);
+      a.result_host = c->res_dev_map;
       ProfScope ps(c, TSS_K_ACCEPT, -1);
       HIPCHK(launch_accept(a, s), "accept");
       ps.done();
@@ -718,7 +766,6 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
       HIPCHK(launch_compact(c->bf16, a, s), "kv compaction");
       ps.done();
     }
-    HIPCHK(hipMemcpyAsync(c->res_host, ws + c->wsl.result, sizeof(Result), hipMemcpyDeviceToHost, s), "result copy");
   }
   HIPCHK(hipStreamSynchronize(s), "step");
   if (c->prof_armed) {

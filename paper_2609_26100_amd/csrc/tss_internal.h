@@ -42,6 +42,7 @@ constexpr int kPage = 16;          // tokens per KV page
 constexpr int kMaxNodes = 64;      // nodes of one verify step (u64 ancestor masks)
 constexpr int kMaxLayers = 256;
 constexpr int kTileBytes = 1024;   // one packed 16 x KC weight tile
+constexpr int kAttnMaxGroups = 16; // workgroups per (head, node tile) in attention
 
 template <typename T> struct Mode;
 template <> struct Mode<__bf16> {
@@ -94,8 +95,9 @@ struct GemmArgs {
   int nkc;                 // K / KC
   // RMSNorm of the A rows: x holds T(h * gain); the row scale
   // rsqrt(sum(h^2) / norm_dim + eps) is applied to the products here.
-  const float* ss_in;      // [ss_nparts][Mp] partial sums of h^2 (null: no norm)
+  const float* ss_in;      // [M][ss_stride] partial sums of h^2, ss_nparts used (null: no norm)
   int ss_nparts;
+  int ss_stride;           // row stride of ss_in / ss_out (parts)
   int norm_dim;
   float eps;
   int Mp;                  // row stride of the partial-sum arrays
@@ -111,14 +113,15 @@ struct GemmArgs {
   void* xn;                // [Mp][N] activation planes of h_new * g_next
   size_t xn_plane;
   const float* g_next;     // gain of the next RMSNorm
-  float* ss_out;           // [N / (16 NT)][Mp] partial sums of h_new^2
+  float* ss_out;           // [M][ss_stride] partial sums of h_new^2, one per strip
   // EPI_SWIGLU
   void* act;               // [Mp][N/2] activation planes of silu(gate) * up
   size_t act_plane;
   // EPI_LOGITS
   float* logits;           // [Mp][N]
-  float* am_val;           // [N / (16 NT)][Mp]
+  float* am_val;           // [M][am_stride] per-strip (max, argmax)
   int32_t* am_idx;
+  int am_stride;
 };
 
 struct AttnArgs {
@@ -126,39 +129,38 @@ struct AttnArgs {
   const uint8_t* kv_pages;
   const int32_t* page_table;
   const StepParams* sp;
-  float* part_o;           // [H][nsplit][Mp][hd]
-  float* part_ml;          // [H][nsplit][Mp][2] (running max in log2 units, sum)
-  int layer, n_pages_pool, n_heads, d, M, Mp;
-  int n_kv, pages_per_split, nsplit;
-  float scale_log2;        // log2(e) / sqrt(hd)
-};
-
-struct CombineArgs {
-  const float* part_o;
-  const float* part_ml;
-  void* o;                 // [Mp][d] activation planes
+  void* o;                 // [Mp][d] activation planes of the attention output
   size_t o_plane;
-  int n_heads, d, M, Mp, nsplit;
+  float* part_o;           // [H * QT][groups][16][hd] unnormalised partial outputs
+  float* part_ml;          // [H * QT][groups][16][2] (max in log2 units, sum)
+  int* counters;           // [H * QT] arrivals, zero between launches
+  int groups;              // workgroups per (head, node tile)
+  int layer, n_pages_pool, n_heads, d, M;
+  int n_kv;
+  float scale_log2;        // log2(e) / sqrt(hd)
 };
 
 struct EmbedArgs {
   const void* embed;       // [V][d] T
-  const StepParams* sp;
+  StepParams sp;           // this step's parameters (by value) ...
+  StepParams* sp_dev;      // ... copied here for the later kernels of the step
   const float* gain;       // gain of the first RMSNorm the rows meet
   float* h;                // [Mp][d]
   void* xn;                // [Mp][d] activation planes
   size_t xn_plane;
-  float* ss_out;           // [1][Mp]
-  int d, M, Mp;
+  float* ss_out;           // [M][ss_stride], part 0
+  int ss_stride;
+  int d, M;
 };
 
 struct AcceptArgs {
-  const float* am_val;     // [nparts][Mp]
+  const float* am_val;     // [M][am_stride]
   const int32_t* am_idx;
-  int nparts, M, Mp;
+  int nparts, M, am_stride;
   const StepParams* sp;
   int32_t* greedy;         // [Mp]
-  Result* result;
+  Result* result;          // device copy (read by the compaction kernel)
+  Result* result_host;     // host-mapped pinned copy (read by the host after the step)
 };
 
 struct CompactArgs {
@@ -172,7 +174,6 @@ struct CompactArgs {
 // Launchers (defined in the .hip files).  T is selected by `bf16`.
 hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attn(bool bf16, int head_dim, int qt, const AttnArgs& a, hipStream_t s);
-hipError_t launch_combine(bool bf16, int head_dim, const CombineArgs& a, hipStream_t s);
 hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_compact(bool bf16, const CompactArgs& a, hipStream_t s);

@@ -1,0 +1,123 @@
+"""GPU checks on the full 7B-shape decoder (32 layers, bf16) in the launch
+configuration the benchmark times (k=5 chains, 1024-token paged context).
+
+* Full depth against the oracle: all 32 layers (dense and the 8-layer skip
+  mask), element-wise logits and the accept decision, at a 64-token context
+  (the oracle's fp32 prefill of 1024 tokens through 32 layers is too slow for a
+  test; every kernel's launch shape except the attention split count is the
+  same at 64 and 1024 tokens).
+* At the benchmark's 1024-token context, properties that hold at any size:
+  the target's own greedy drafts are fully accepted, steps are bit-exact run
+  to run, a chain passed as an explicit parent array is bit-exact with the
+  implicit chain, and a skip mask is bit-identical to the model with the
+  skipped blocks deleted.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import OracleSequence, prefill, verify
+from tests.gpu_common import compare_step, gpu_verifier, log, oracle_model
+
+pytestmark = pytest.mark.gpu
+
+SHAPE = synth.LLAMA_7B
+L = SHAPE.n_layers
+CTX = 1024
+MASKS = synth.nested_skip_masks(L, 16, 31, (0, 4, 8))
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    log("generating and loading the 7B-shape bf16 model")
+    v = gpu_verifier(SHAPE, n_seqs=2, max_tokens=CTX + 80, max_nodes=64)
+    yield v
+    v.close()
+
+
+@pytest.fixture(scope="module")
+def oracle7b():
+    return oracle_model(SHAPE)
+
+
+@pytest.mark.parametrize("skips", [0, 8])
+def test_full_depth_vs_oracle(gpu, oracle7b, skips):
+    v, m = gpu, oracle7b
+    mask = MASKS[skips]
+    toks = synth.context_tokens(SHAPE.vocab, 64 + 4, stream=30 + skips)
+    ctx = toks[:64]
+    v.truncate(1, 0)
+    v.set_mask(1, mask)
+    v.prefill(1, ctx)
+    o = OracleSequence(m, mask)
+    prefill(m, o, ctx)
+    compared, worst = 0, 0.0
+    for r in range(3):
+        root = int(toks[64 + r])
+        g, cur = [], [root]
+        for _ in range(5):
+            g.append(int(verify(m, o, np.asarray(cur)).greedy[-1]))
+            cur.append(g[-1])
+        drafts = synth.chain_draft(np.asarray(g), SHAPE.vocab, p_accept=0.6, stream=r)
+        res, (al, nt), err, c = compare_step(SHAPE, v, 1, m, o, np.concatenate([[root], drafts]))
+        compared += c
+        worst = max(worst, err)
+        log(f"32 layers skip {skips} root {r}: accept {al}/{res.accept_len} next {nt}/{res.next_token} err {err:.3e}")
+    log(f"32 layers skip {skips}: worst logits max-abs {worst:.3e}, {compared}/3 decisions compared")
+    assert compared >= 1
+
+
+def _prepare(v, mask):
+    toks = synth.context_tokens(SHAPE.vocab, CTX + 1)
+    v.truncate(0, 0)
+    v.set_mask(0, mask)
+    v.prefill(0, toks[:CTX])
+    return int(toks[CTX])
+
+
+@pytest.mark.parametrize("skips", [0, 4, 8])
+def test_own_greedy_fully_accepted_and_deterministic(gpu, skips):
+    v = gpu
+    root = _prepare(v, MASKS[skips])
+    cur = [root]
+    for _ in range(6):
+        v.verify(0, cur)
+        cur.append(int(v.greedy(len(cur))[-1]))
+    outs = []
+    for _ in range(3):
+        al, nt = v.verify(0, cur[:6])
+        assert (al, nt) == (5, cur[6])
+        outs.append(v.logits(6))
+    np.testing.assert_array_equal(outs[0], outs[1])
+    np.testing.assert_array_equal(outs[0], outs[2])
+    b = v.verify(0, cur[:6], np.arange(-1, 5, dtype=np.int32))
+    assert b == (5, cur[6])
+    np.testing.assert_array_equal(v.logits(6), outs[0])
+    assert v.length(0) == CTX
+
+
+def test_skip_mask_equals_deleted_blocks(gpu):
+    """Mask of 8 skipped layers == the 24-layer model made of the active blocks, bit for bit."""
+    import dataclasses
+
+    from paper_2609_26100_amd.verifier import Verifier
+    v = gpu
+    mask = MASKS[8]
+    active = [l for l in range(L) if not mask[l]]
+    short = dataclasses.replace(SHAPE, n_layers=len(active))
+    names = {i: (ly, nm) for i, ly, nm in synth.tensor_names(short.n_layers)}
+
+    def get(idx):
+        ly, nm = names[idx]
+        return synth.weight_tensor(SHAPE, nm, active[ly] if ly >= 0 else -1, as_bf16_bits=True)
+    log("loading the 24-layer model")
+    w = Verifier(short, n_seqs=1, max_tokens=CTX + 80, max_nodes=64)
+    w.load(get)
+    root = _prepare(v, mask)
+    w.prefill(0, synth.context_tokens(SHAPE.vocab, CTX + 1)[:CTX])
+    tok = np.concatenate([[root], synth.context_tokens(SHAPE.vocab, 5, stream=40)])
+    a = v.verify(0, tok)
+    b = w.verify(0, tok)
+    assert a == b
+    np.testing.assert_array_equal(v.logits(6), w.logits(6))
+    w.close()
