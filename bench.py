@@ -89,6 +89,7 @@ def run_gpu(args):
 
     results = {}
     prof = None
+    direct_median = None
     for s in args.skips:
         mask = masks[s]
         v.truncate(0, 0)
@@ -104,29 +105,38 @@ def run_gpu(args):
         log(f"skip {s}: layers {np.nonzero(mask)[0].tolist()} prefill+greedy {time.time() - t1:.1f}s")
         drafts = [np.concatenate([[root], synth.chain_draft(greedy, shape.vocab, p_accept=P_ACCEPT, stream=i)])
                   for i in range(args.warmup + args.steps)]
-        for i in range(args.warmup):
-            v.verify(0, drafts[i], commit=True)
-            v.truncate(0, CTX)
+        def timed(n_steps, tag, after_warmup=None):
+            for i in range(args.warmup):
+                v.verify(0, drafts[i], commit=True)
+                v.truncate(0, CTX)
+            if after_warmup:
+                after_warmup()
+            log(f"skip {s}: timing {n_steps} steps ({tag})")
+            torch.cuda.synchronize()
+            lat = np.empty(n_steps)
+            acc = np.empty(n_steps, dtype=np.int64)
+            t_start = time.perf_counter()
+            for i in range(n_steps):
+                a = time.perf_counter()
+                al, _ = v.verify(0, drafts[args.warmup + i], commit=True)
+                lat[i] = time.perf_counter() - a
+                acc[i] = al
+                v.truncate(0, CTX)
+            torch.cuda.synchronize()
+            return lat, acc, time.perf_counter() - t_start
+
+        v.set_launch_mode(abi.TSS_LAUNCH_GRAPH)
+        lat, acc, total = timed(args.steps, "graph launches")
         if s == 0:
+            # the gate/up kernel timed with HIP events (these steps use direct launches)
+            v.set_launch_mode(abi.TSS_LAUNCH_DIRECT)
             abi.tss_profile_kernel(v.ctx, abi.TSS_K_GATEUP, 0)
-            abi.tss_profile_read(v.ctx, reset=True)
-        log(f"skip {s}: timing {args.steps} steps")
-        torch.cuda.synchronize()
-        lat = np.empty(args.steps)
-        acc = np.empty(args.steps, dtype=np.int64)
-        t_start = time.perf_counter()
-        for i in range(args.steps):
-            a = time.perf_counter()
-            al, _ = v.verify(0, drafts[args.warmup + i], commit=True)
-            lat[i] = time.perf_counter() - a
-            acc[i] = al
-            v.truncate(0, CTX)
-        torch.cuda.synchronize()
-        total = time.perf_counter() - t_start
-        if s == 0:
-            ms, n = abi.tss_profile_read(v.ctx, reset=True)
+            dlat, _, _ = timed(args.steps, "direct launches, gate/up kernel timed with events",
+                               after_warmup=lambda: abi.tss_profile_read(v.ctx, reset=True))
+            prof = abi.tss_profile_read(v.ctx, reset=True)
             abi.tss_profile_kernel(v.ctx, -1)
-            prof = (ms, n)
+            v.set_launch_mode(abi.TSS_LAUNCH_GRAPH)
+            direct_median = float(np.median(dlat))
         active = shape.n_layers - s
         by = algorithmic_bytes(shape, active, CTX, M)
         med = float(np.median(lat))
@@ -142,6 +152,8 @@ def run_gpu(args):
             "roofline_frac": by / PEAK_HBM / med,
             "wall_s": total,
         }
+        if s == 0:
+            results[s]["latency_us_median_direct_launches"] = direct_median * 1e6
         log(f"skip {s}: median {med * 1e6:.0f} us, accepted {results[s]['accepted_tok_s']:.0f} tok/s, "
             f"roofline frac {results[s]['roofline_frac']:.3f}")
     d0 = results[args.skips[0]]

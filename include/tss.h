@@ -66,6 +66,15 @@ enum tss_flags {
   TSS_COMMIT = 1u      /* keep the K/V of the root and the accepted path; n_kv += accept_len + 1 */
 };
 
+/* How tss_verify issues its kernels (tss_set_launch_mode). */
+enum tss_launch_mode {
+  TSS_LAUNCH_DIRECT = 0, /* one launch per kernel */
+  TSS_LAUNCH_GRAPH = 1   /* default: the step's launches are captured once per step shape
+                            (sequence, skip mask, node count, tree or chain, attention
+                            workgroups) into a HIP graph and replayed; results are
+                            bit-identical to direct launches */
+};
+
 /* Kernel kinds for tss_profile_kernel. */
 enum tss_kernel {
   TSS_K_EMBED = 0,
@@ -83,8 +92,11 @@ enum tss_kernel {
  *   d_model == n_heads * head_dim; head_dim in {64, 128};
  *   d_model and ffn_dim multiples of 32; vocab a multiple of 32;
  *   1 <= max_nodes <= 64 (nodes of one verify, root included);
- *   dtype TSS_BF16 (bf16 weights, KV and GEMM inputs; fp32 accumulation,
- *   residual stream, softmax and logits) or TSS_F32 (everything fp32).
+ *   d_model <= 8192;
+ *   dtype TSS_BF16 (bf16 weights; fp16 KV cache and attention operands; fp32
+ *   activations fed to the projections as bf16 hi/lo pairs; fp32
+ *   accumulation, residual stream, softmax and logits) or TSS_F32 (everything
+ *   fp32).
  * The KV page size is fixed at 16 tokens. */
 typedef struct {
   int32_t n_layers;
@@ -171,9 +183,17 @@ int tss_validate_mask(const uint8_t* mask, int32_t n_layers);
 /* depth[i] and anc[i] (bit j set iff node j is i or an ancestor of i). */
 int tss_tree_meta(const int32_t* parent, int32_t n_nodes, int32_t* depth, uint64_t* anc);
 
-/* Times one kernel launch per verify with HIP events on the context's stream:
- * the launch of kind `kernel` (enum tss_kernel) for layer `layer` (ignored for
- * kinds outside the layer loop).  kernel = -1 switches timing off.
+/* Selects the launch mode of tss_verify (enum tss_launch_mode).  At most 32
+ * captured step shapes are kept per context (least recently used dropped). */
+int tss_set_launch_mode(tss_ctx* ctx, int32_t mode);
+
+/* Times one kernel launch per verify: the launch of kind `kernel` (enum
+ * tss_kernel) for layer `layer` (ignored for kinds outside the layer loop);
+ * kernel = -1 switches timing off.  Two HIP events are bound to that launch's
+ * own dispatch (hipExtLaunchKernel), so they hold the start and end of the
+ * kernel's execution, the figure a kernel-trace profiler reports, with no
+ * event-record overhead between them.  While timing is on, verify steps use
+ * direct launches (a captured graph cannot carry the events).
  * tss_profile_read returns the summed milliseconds and the launch count
  * (reset != 0 clears them). */
 int tss_profile_kernel(tss_ctx* ctx, int32_t kernel, int32_t layer);

@@ -53,7 +53,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 
   const int head = blockIdx.x, qt = blockIdx.y, g = blockIdx.z, G = gridDim.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r16 = lane & 15, grp = lane >> 4;
-  const int M = a.M, n_kv = a.n_kv;
+  const int M = a.M, n_kv = a.sp->n_kv;
   const int qn = qt * 16 + r16;
 
   // B operand of S = K Q^T: lane (node qn, group grp) holds q[qn][head*HD + grp*DL + 0..DL).
@@ -88,7 +88,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 
   const size_t blk_elems = 16 * (size_t)HD;
   auto load_page = [&](int p, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
-    const int phys = a.page_table[p];
+    const int phys = p < kArgPages ? a.pages[p] : a.page_table[p];  // p is uniform across the wave
     const TK* kb = (const TK*)a.kv_pages + (((size_t)a.layer * a.n_pages_pool + phys) * 2 * a.n_heads + head) * blk_elems;
     const TK* vb = kb + (size_t)a.n_heads * blk_elems;
     const uint4* kp = (const uint4*)(kb + r16 * HD + grp * DL);
@@ -202,9 +202,27 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     for (int v = 0; v < 4; ++v) sm_o[(wave * 64 + lane) * OS + n * 4 + v] = O[n][v];
   __syncthreads();
 
-  // Workgroup state: per row (m, l) and per output position the unnormalised
-  // sum.  Output position e = (source lane, n, v): node row 4*(lane/16)+v,
-  // dim NO*(lane%16)+n.
+  // Row factors once: mx = max_w m_w, f_w = 2^(m_w - mx), den = sum_w f_w l_w.
+  float* sm_mx = sm_o + W * 64 * OS;      // [16]
+  float* sm_f = sm_mx + 16;               // [W][16]
+  float* sm_den = sm_f + W * 16;          // [16]
+  if (threadIdx.x < 16) {
+    float mx = -1e30f;
+    for (int w = 0; w < W; ++w) mx = fmaxf(mx, sm_m[w * 16 + threadIdx.x]);
+    sm_mx[threadIdx.x] = mx;
+  }
+  __syncthreads();
+  if (threadIdx.x < W * 16) sm_f[threadIdx.x] = exp2f(sm_m[threadIdx.x] - sm_mx[threadIdx.x & 15]);
+  __syncthreads();
+  if (threadIdx.x < 16) {
+    float den = 0.f;
+    for (int w = 0; w < W; ++w) den += sm_f[w * 16 + threadIdx.x] * sm_l[w * 16 + threadIdx.x];
+    sm_den[threadIdx.x] = den;
+  }
+  __syncthreads();
+
+  // Output position e = (source lane, n, v): node row 4*(lane/16)+v, dim
+  // NO*(lane%16)+n; its value is sum_w f_w O_w (unnormalised) in wave order.
   const size_t tile = (size_t)head * gridDim.y + qt;       // (head, node tile)
   float* pm = a.part_ml + (tile * G + g) * 32;             // [16][2]
   float* po = a.part_o + (tile * G + g) * 16 * HD;         // [16][HD]
@@ -213,24 +231,17 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     const int row = (src >> 4) * 4 + v;
     const int node = qt * 16 + row;
     if (node >= M) continue;
-    float mx = -1e30f;
-    for (int w = 0; w < W; ++w) mx = fmaxf(mx, sm_m[w * 16 + row]);
-    float num = 0.f, den = 0.f;
-    for (int w = 0; w < W; ++w) {
-      const float f = exp2f(sm_m[w * 16 + row] - mx);
-      den += f * sm_l[w * 16 + row];
-      num += f * sm_o[(w * 64 + src) * OS + n * 4 + v];
-    }
+    float num = 0.f;
+    for (int w = 0; w < W; ++w) num += sm_f[w * 16 + row] * sm_o[(w * 64 + src) * OS + n * 4 + v];
     const int dim = NO * (src & 15) + n;
-    if (G == 1) {
-      store_act<TW>(a.o, a.o_plane, (size_t)node * a.d + head * HD + dim, num / den);
-    } else {
+    if (G == 1)
+      store_act<TW>(a.o, a.o_plane, (size_t)node * a.d + head * HD + dim, num / sm_den[row]);
+    else
       po[row * HD + dim] = num;
-      if ((src & 15) == 0 && n == 0) {  // one writer per row: source lane 16 * (row / 4), n = 0
-        pm[row * 2 + 0] = mx;
-        pm[row * 2 + 1] = den;
-      }
-    }
+  }
+  if (G > 1 && threadIdx.x < 16) {
+    pm[threadIdx.x * 2 + 0] = sm_mx[threadIdx.x];
+    pm[threadIdx.x * 2 + 1] = sm_den[threadIdx.x];
   }
   if (G == 1) return;
 
@@ -268,19 +279,32 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   if (threadIdx.x == 0) a.counters[tile] = 0;
 }
 
+template <typename TK, int HD>
+constexpr size_t attn_lds() {
+  return (size_t)(64 * (HD / 4 * (int)sizeof(TK) / 16) * 4 + kAttnWaves * 16 * 2 + kAttnWaves * 64 * (HD / 4 + 1) +
+                  16 + kAttnWaves * 16 + 16) * 4;
+}
+
+template <typename TK, typename TW, int HD>
+static hipError_t attn_attr() {
+  return hipFuncSetAttribute((const void*)k_attn<TK, TW, HD>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)attn_lds<TK, HD>());
+}
+
+// Raises the LDS limit of the attention kernels (more than 64 KiB); done once
+// at context creation so that no attribute call falls inside a captured step.
+hipError_t init_kernel_attributes() {
+  hipError_t e = attn_attr<_Float16, __bf16, 128>();
+  if (e == hipSuccess) e = attn_attr<_Float16, __bf16, 64>();
+  if (e == hipSuccess) e = attn_attr<float, float, 128>();
+  if (e == hipSuccess) e = attn_attr<float, float, 64>();
+  return e;
+}
+
 template <typename TK, typename TW, int HD>
 static hipError_t attn_t(int qt, const AttnArgs& a, hipStream_t s) {
-  constexpr int NO = HD / 16;
-  constexpr int NQ = HD / 4 * (int)sizeof(TK) / 16;
-  const size_t lds = (size_t)(64 * NQ * 4 + kAttnWaves * 16 * 2 + kAttnWaves * 64 * (NO * 4 + 1)) * 4;
-  static bool attr = false;
-  if (!attr) {
-    const hipError_t e = hipFuncSetAttribute((const void*)k_attn<TK, TW, HD>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
-  hipLaunchKernelGGL((k_attn<TK, TW, HD>), dim3(a.n_heads, qt, a.groups), dim3(kAttnWaves * 64), lds, s, a);
+  const size_t lds = attn_lds<TK, HD>();
+  TSS_LAUNCH((k_attn<TK, TW, HD>), dim3(a.n_heads, qt, a.groups), dim3(kAttnWaves * 64), lds, s, a);
   return hipGetLastError();
 }
 

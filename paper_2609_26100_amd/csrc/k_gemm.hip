@@ -205,7 +205,8 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
         a.q[(size_t)row * d + head * HD + dim] = val;
       } else {
         const int slot = n_kv + row;
-        const int page = a.page_table[slot >> 4];
+        const int lp = slot >> 4;
+        const int page = lp < kArgPages ? a.pages[lp] : a.page_table[lp];
         const int tin = slot & 15;
         KV* blk = (KV*)a.kv_pages +
                   ((((size_t)a.layer * a.n_pages_pool + page) * 2 + (sec - 1)) * a.n_heads + head) * (16 * (size_t)HD);
@@ -273,10 +274,10 @@ static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
   const size_t lds = (size_t)(waves * rows * cols + rows * cols * 2 + rows) * 4;
   dim3 grid(strips), block(waves * 64);
   switch (epi) {
-    case EPI_QKV: hipLaunchKernelGGL((k_gemm<T, MT, 1, EPI_QKV>), grid, block, lds, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((k_gemm<T, MT, 1, EPI_RESID>), grid, block, lds, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((k_gemm<T, MT, 2, EPI_SWIGLU>), grid, block, lds, s, a); break;
-    default: hipLaunchKernelGGL((k_gemm<T, MT, 1, EPI_LOGITS>), grid, block, lds, s, a); break;
+    case EPI_QKV: TSS_LAUNCH((k_gemm<T, MT, 1, EPI_QKV>), grid, block, lds, s, a); break;
+    case EPI_RESID: TSS_LAUNCH((k_gemm<T, MT, 1, EPI_RESID>), grid, block, lds, s, a); break;
+    case EPI_SWIGLU: TSS_LAUNCH((k_gemm<T, MT, 2, EPI_SWIGLU>), grid, block, lds, s, a); break;
+    default: TSS_LAUNCH((k_gemm<T, MT, 1, EPI_LOGITS>), grid, block, lds, s, a); break;
   }
   return hipGetLastError();
 }

@@ -153,6 +153,7 @@ template <typename T>
 __global__ __launch_bounds__(128) void k_compact(CompactArgs a) {
   const int layer = blockIdx.x, head = blockIdx.y, dim = threadIdx.x;
   if (a.sp->mask[layer] || dim >= a.head_dim) return;
+  const int n_kv = a.sp->n_kv;
   const int len = a.result->accept_len;
   const int HD = a.head_dim;
   T kbuf[kMaxNodes], vbuf[kMaxNodes];
@@ -167,14 +168,14 @@ __global__ __launch_bounds__(128) void k_compact(CompactArgs a) {
     return blk + (tin >> 2) * HD * 4 + dim * 4 + (tin & 3);
   };
   for (int d = 1; d <= len; ++d) {
-    const int src = a.n_kv + a.result->path[d];
+    const int src = n_kv + a.result->path[d];
     kbuf[d] = *kaddr(src);
     vbuf[d] = *vaddr(src);
   }
   for (int d = 1; d <= len; ++d) {
     if (a.result->path[d] == d) continue;
-    *kaddr(a.n_kv + d) = kbuf[d];
-    *vaddr(a.n_kv + d) = vbuf[d];
+    *kaddr(n_kv + d) = kbuf[d];
+    *vaddr(n_kv + d) = vbuf[d];
   }
 }
 
@@ -189,30 +190,34 @@ __global__ void k_rope_table(float2* tab, int max_pos, int head_dim, float base)
   tab[i] = make_float2((float)cos(ang), (float)sin(ang));
 }
 
+const void* embed_kernel(bool bf16) {
+  return bf16 ? (const void*)k_embed<__bf16> : (const void*)k_embed<float>;
+}
+
 hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s) {
   if (bf16)
-    hipLaunchKernelGGL(k_embed<__bf16>, dim3(a.M), dim3(256), 0, s, a);
+    TSS_LAUNCH(k_embed<__bf16>, dim3(a.M), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(k_embed<float>, dim3(a.M), dim3(256), 0, s, a);
+    TSS_LAUNCH(k_embed<float>, dim3(a.M), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_accept, dim3(1), dim3(1024), 0, s, a);
+  TSS_LAUNCH(k_accept, dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_compact(bool bf16, const CompactArgs& a, hipStream_t s) {
   if (bf16)
-    hipLaunchKernelGGL(k_compact<_Float16>, dim3(a.n_layers, a.n_heads), dim3(128), 0, s, a);
+    TSS_LAUNCH(k_compact<_Float16>, dim3(a.n_layers, a.n_heads), dim3(128), 0, s, a);
   else
-    hipLaunchKernelGGL(k_compact<float>, dim3(a.n_layers, a.n_heads), dim3(128), 0, s, a);
+    TSS_LAUNCH(k_compact<float>, dim3(a.n_layers, a.n_heads), dim3(128), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base, hipStream_t s) {
   const int n = max_pos * (head_dim >> 1);
-  hipLaunchKernelGGL(k_rope_table, dim3((n + 255) / 256), dim3(256), 0, s, tab, max_pos, head_dim, base);
+  TSS_LAUNCH(k_rope_table, dim3((n + 255) / 256), dim3(256), 0, s, tab, max_pos, head_dim, base);
   return hipGetLastError();
 }
 

@@ -20,6 +20,13 @@
 
 using namespace tss;
 
+namespace tss {
+LaunchTiming& launch_timing() {
+  static thread_local LaunchTiming t;
+  return t;
+}
+}  // namespace tss
+
 namespace {
 
 constexpr size_t kStageBytes = 32u << 20;  // one pinned weight-upload buffer
@@ -144,6 +151,7 @@ struct tss_ctx {
   KvLayout kvl;
   int n_seqs = 0, max_tokens = 0;
   std::vector<int32_t> n_kv;
+  std::vector<int32_t> pt_host;   // host copy of the page tables
   std::vector<std::vector<int32_t>> kv_len;
   std::vector<std::vector<uint8_t>> mask;
   // pinned host staging: step parameters and result, and two weight-upload
@@ -157,6 +165,20 @@ struct tss_ctx {
   int last_M = 0;
   bool poisoned = false;
   std::string err;
+  // verify steps replayed from captured HIP graphs, keyed by the step's shape
+  struct GraphEntry {
+    std::string key;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    hipGraphNode_t embed_node = nullptr;
+    hipKernelNodeParams embed_params{};
+    uint64_t last_use = 0;
+  };
+  int launch_mode = TSS_LAUNCH_GRAPH;
+  hipStream_t cap_stream = nullptr;
+  std::vector<GraphEntry> graphs;
+  uint64_t graph_clock = 0;
+  hipStream_t cur_stream = nullptr;  // stream the launches of the current step go to
   // one-launch event timing
   int prof_kind = -1, prof_layer = -1;
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
@@ -323,6 +345,7 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
   if (e == hipSuccess) e = hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * (c->Mp / 16) * 4,
                                           c->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e == hipSuccess) e = init_kernel_attributes();
   if (e == hipSuccess) e = hipEventCreate(&c->ev0);
   if (e == hipSuccess) e = hipEventCreate(&c->ev1);
   if (e != hipSuccess) {
@@ -335,6 +358,11 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
 
 void tss_destroy(tss_ctx* c) {
   if (!c) return;
+  for (auto& g : c->graphs) {
+    if (g.exec) (void)hipGraphExecDestroy(g.exec);
+    if (g.graph) (void)hipGraphDestroy(g.graph);
+  }
+  if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
   for (int i = 0; i < 2; ++i) {
     if (c->stage_ev[i]) {
       (void)hipEventSynchronize(c->stage_ev[i]);
@@ -485,6 +513,7 @@ int tss_kv_alloc(tss_ctx* c, int32_t n_seqs, int32_t max_tokens_per_seq, void* d
   c->n_seqs = n_seqs;
   c->max_tokens = max_tokens_per_seq;
   HIPCHK(hipMemcpy(c->kv + k.page_table, pt.data(), pt.size() * 4, hipMemcpyHostToDevice), "page table upload");
+  c->pt_host = pt;
   HIPCHK(launch_rope_table((float2*)(c->kv + k.rope), max_tokens_per_seq, c->cfg.head_dim, c->cfg.rope_base,
                            c->stream),
          "rope table");
@@ -519,6 +548,13 @@ int tss_seq_truncate(tss_ctx* c, int32_t seq, int32_t n_kv) {
   return TSS_OK;
 }
 
+int tss_set_launch_mode(tss_ctx* c, int32_t mode) {
+  if (!c) return TSS_EINVAL;
+  if (mode != TSS_LAUNCH_DIRECT && mode != TSS_LAUNCH_GRAPH) return fail(c, TSS_EINVAL, "unknown launch mode");
+  c->launch_mode = mode;
+  return TSS_OK;
+}
+
 int tss_profile_kernel(tss_ctx* c, int32_t kernel, int32_t layer) {
   if (!c) return TSS_EINVAL;
   if (kernel < -1 || kernel > TSS_K_COMPACT) return fail(c, TSS_EINVAL, "unknown kernel kind");
@@ -542,27 +578,38 @@ int tss_profile_read(tss_ctx* c, double* total_ms, int64_t* count, int32_t reset
 
 namespace {
 
-// Brackets one launch with events when it is the profiled one.
+// Binds the context's event pair to one launch when it is the profiled one.
 struct ProfScope {
   tss_ctx* c;
   bool on;
   ProfScope(tss_ctx* ctx, int kind, int layer) : c(ctx) {
     on = c->prof_kind == kind && (layer < 0 || c->prof_layer == layer) && !c->prof_armed;
-    if (on) {
-      (void)hipEventRecord(c->ev0, c->stream);
-    }
+    if (on) launch_timing() = LaunchTiming{c->ev0, c->ev1};
   }
   void done() {
     if (on) {
-      (void)hipEventRecord(c->ev1, c->stream);
+      launch_timing() = LaunchTiming{};
       c->prof_armed = true;
     }
   }
+  ~ProfScope() {
+    if (on) launch_timing() = LaunchTiming{};
+  }
 };
 
-// Runs embed, the active blocks and (for verify) lm_head + accept for the
-// nodes already in c->sp_host.  seq's page table is used for KV.
-int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
+EmbedArgs embed_args(tss_ctx* c);
+
+int attn_groups_for(int n_kv, int M) {
+  const int n_pages = (n_kv + M + kPage - 1) / kPage;
+  return std::max(1, std::min(kAttnMaxGroups, (n_pages + 15) / 16));
+}
+
+// Enqueues embed, the active blocks and (for verify) lm_head + accept for the
+// nodes in c->sp_host on stream s.  seq's page table is used for KV.  Every
+// kernel argument except the embedding kernel's step parameters depends only
+// on (seq, mask, node count, tree/chain, attention groups), so a captured
+// sequence can be replayed for later steps of the same shape.
+int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) {
   const tss_model_cfg& cf = c->cfg;
   const StepParams& sp = *c->sp_host;
   const int M = sp.M, L = cf.n_layers, d = cf.d_model, f = cf.ffn_dim, H = cf.n_heads, hd = cf.head_dim;
@@ -570,9 +617,10 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
   uint8_t* ws = c->ws;
   StepParams* sp_dev = (StepParams*)(ws + c->wsl.sp);
   const int32_t* pt = (const int32_t*)(c->kv + c->kvl.page_table) + (size_t)seq * c->kvl.pages_per_seq;
+  const int32_t* pt_h = c->pt_host.data() + (size_t)seq * c->kvl.pages_per_seq;
   uint8_t* pages = c->kv + c->kvl.pages;
   const float2* rope = (const float2*)(c->kv + c->kvl.rope);
-  hipStream_t s = c->stream;
+  c->cur_stream = s;
 
   std::vector<int> active;
   for (int l = 0; l < L; ++l)
@@ -584,18 +632,7 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
   c->prof_armed = false;
 
   {
-    EmbedArgs a{};
-    a.embed = c->w + c->wl.embed;
-    a.sp = sp;
-    a.sp_dev = sp_dev;
-    a.gain = attn_gain(0);
-    a.h = (float*)(ws + c->wsl.h);
-    a.xn = ws + c->wsl.xa;
-    a.xn_plane = act_planes(&cf) == 2 ? (size_t)c->Mp * d : 0;
-    a.ss_out = (float*)(ws + c->wsl.ss_a);
-    a.ss_stride = d / 16;
-    a.d = d;
-    a.M = M;
+    const EmbedArgs a = embed_args(c);
     ProfScope ps(c, TSS_K_EMBED, -1);
     HIPCHK(launch_embed(c->bf16, a, s), "embed");
     ps.done();
@@ -614,8 +651,7 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
 
   // attention: one page per wave where possible, at most kAttnMaxGroups
   // sixteen-wave workgroups per (head, node tile)
-  const int n_pages = (sp.n_kv + M + kPage - 1) / kPage;
-  const int attn_groups = std::max(1, std::min(kAttnMaxGroups, (n_pages + 15) / 16));
+  const int attn_groups = attn_groups_for(sp.n_kv, M);
 
   for (size_t idx = 0; idx < active.size(); ++idx) {
     const int l = active[idx];
@@ -633,6 +669,7 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
       a.q = (float*)(ws + c->wsl.q);
       a.kv_pages = pages;
       a.page_table = pt;
+      for (int i = 0; i < kArgPages; ++i) a.pages[i] = i < c->kvl.pages_per_seq ? pt_h[i] : 0;
       a.rope = rope;
       a.layer = l;
       a.n_pages_pool = c->kvl.n_pages;
@@ -651,6 +688,7 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
       a.sp = sp_dev;
       a.o = ws + c->wsl.o;
       a.o_plane = plane_d;
+      for (int i = 0; i < kArgPages; ++i) a.pages[i] = i < c->kvl.pages_per_seq ? pt_h[i] : 0;
       a.part_o = (float*)(ws + c->wsl.part_o);
       a.part_ml = (float*)(ws + c->wsl.part_ml);
       a.counters = (int*)(ws + c->wsl.counters);
@@ -660,7 +698,6 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
       a.n_heads = H;
       a.d = d;
       a.M = M;
-      a.n_kv = sp.n_kv;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
       ProfScope ps(c, TSS_K_ATTN, l);
       HIPCHK(launch_attn(c->bf16, hd, mt, a, s), "attention");
@@ -761,13 +798,17 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
       a.n_pages_pool = c->kvl.n_pages;
       a.n_heads = H;
       a.head_dim = hd;
-      a.n_kv = sp.n_kv;
       ProfScope ps(c, TSS_K_COMPACT, -1);
       HIPCHK(launch_compact(c->bf16, a, s), "kv compaction");
       ps.done();
     }
   }
-  HIPCHK(hipStreamSynchronize(s), "step");
+  return TSS_OK;
+}
+
+// Waits for the step and collects the profiled launch's event times.
+int finish_step(tss_ctx* c) {
+  HIPCHK(hipStreamSynchronize(c->stream), "step");
   if (c->prof_armed) {
     float ms = 0.f;
     HIPCHK(hipEventElapsedTime(&ms, c->ev0, c->ev1), "event timing");
@@ -776,6 +817,112 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
     c->prof_armed = false;
   }
   return TSS_OK;
+}
+
+int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
+  const int r = enqueue_step(c, seq, verify, compact, c->stream);
+  if (r) return r;
+  return finish_step(c);
+}
+
+// The embedding kernel's arguments for the step in c->sp_host (the only
+// per-step arguments of a verify).
+EmbedArgs embed_args(tss_ctx* c) {
+  const tss_model_cfg& cf = c->cfg;
+  const StepParams& sp = *c->sp_host;
+  int first = -1;
+  for (int l = 0; l < cf.n_layers && first < 0; ++l)
+    if (!sp.mask[l]) first = l;
+  EmbedArgs a{};
+  a.embed = c->w + c->wl.embed;
+  a.sp = sp;
+  a.sp_dev = (StepParams*)(c->ws + c->wsl.sp);
+  a.gain = (const float*)(c->w + (first >= 0 ? c->wl.layers[first].attn_norm : c->wl.final_norm));
+  a.h = (float*)(c->ws + c->wsl.h);
+  a.xn = c->ws + c->wsl.xa;
+  a.xn_plane = act_planes(&cf) == 2 ? (size_t)c->Mp * cf.d_model : 0;
+  a.ss_out = (float*)(c->ws + c->wsl.ss_a);
+  a.ss_stride = cf.d_model / 16;
+  a.d = cf.d_model;
+  a.M = sp.M;
+  return a;
+}
+
+// A verify step from the graph cache: captured on first use of its shape,
+// then replayed with the embedding kernel's step parameters updated.
+int run_verify_graph(tss_ctx* c, int seq, bool compact) {
+  const StepParams& sp = *c->sp_host;
+  std::string key;
+  key.reserve(64 + c->cfg.n_layers);
+  auto put = [&](int v) { key.append((const char*)&v, sizeof(v)); };
+  put(seq);
+  put(sp.M);
+  put(compact);
+  put(attn_groups_for(sp.n_kv, sp.M));
+  key.append((const char*)sp.mask, c->cfg.n_layers);
+  tss_ctx::GraphEntry* g = nullptr;
+  for (auto& e : c->graphs)
+    if (e.key == key) g = &e;
+  if (!g) {
+    constexpr size_t kMaxGraphs = 32;
+    if (c->graphs.size() >= kMaxGraphs) {  // drop the least recently used
+      size_t old = 0;
+      for (size_t i = 1; i < c->graphs.size(); ++i)
+        if (c->graphs[i].last_use < c->graphs[old].last_use) old = i;
+      HIPCHK(hipGraphExecDestroy(c->graphs[old].exec), "graph destroy");
+      HIPCHK(hipGraphDestroy(c->graphs[old].graph), "graph destroy");
+      c->graphs.erase(c->graphs.begin() + old);
+    }
+    if (!c->cap_stream) HIPCHK(hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking), "capture stream");
+    tss_ctx::GraphEntry e;
+    e.key = key;
+    c->prof_armed = false;
+    HIPCHK(hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal), "begin capture");
+    const int r = enqueue_step(c, seq, true, compact, c->cap_stream);
+    hipGraph_t graph = nullptr;
+    const hipError_t ce = hipStreamEndCapture(c->cap_stream, &graph);
+    if (r) {
+      if (graph) (void)hipGraphDestroy(graph);
+      return r;
+    }
+    HIPCHK(ce, "end capture");
+    e.graph = graph;
+    c->prof_armed = false;
+    HIPCHK(hipGraphInstantiate(&e.exec, graph, nullptr, nullptr, 0), "graph instantiate");
+    size_t n = 0;
+    HIPCHK(hipGraphGetNodes(graph, nullptr, &n), "graph nodes");
+    std::vector<hipGraphNode_t> nodes(n);
+    HIPCHK(hipGraphGetNodes(graph, nodes.data(), &n), "graph nodes");
+    const void* ek = embed_kernel(c->bf16);
+    for (auto node : nodes) {
+      hipGraphNodeType t;
+      HIPCHK(hipGraphNodeGetType(node, &t), "graph node type");
+      if (t != hipGraphNodeTypeKernel) continue;
+      hipKernelNodeParams kp{};
+      HIPCHK(hipGraphKernelNodeGetParams(node, &kp), "graph node params");
+      if (kp.func == ek) {
+        e.embed_node = node;
+        e.embed_params = kp;
+        break;
+      }
+    }
+    if (!e.embed_node) {
+      (void)hipGraphExecDestroy(e.exec);
+      (void)hipGraphDestroy(graph);
+      return fail(c, TSS_EHIP, "captured step has no embedding launch");
+    }
+    c->graphs.push_back(e);
+    g = &c->graphs.back();
+  }
+  g->last_use = ++c->graph_clock;
+  EmbedArgs a = embed_args(c);
+  void* kargs[1] = {&a};
+  hipKernelNodeParams kp = g->embed_params;
+  kp.kernelParams = kargs;
+  kp.extra = nullptr;
+  HIPCHK(hipGraphExecKernelNodeSetParams(g->exec, g->embed_node, &kp), "graph update");
+  HIPCHK(hipGraphLaunch(g->exec, c->stream), "graph launch");
+  return finish_step(c);
 }
 
 int check_ready(tss_ctx* c, int seq) {
@@ -860,7 +1007,10 @@ int tss_verify(tss_ctx* c, int32_t seq, const int32_t* draft_tokens, const int32
   bool is_chain = true;
   for (int i = 1; i < n_nodes; ++i)
     if (sp.parent[i] != i - 1) is_chain = false;
-  r = run_step(c, seq, true, commit && !is_chain);
+  // event timing of one launch needs direct launches (events recorded inside a
+  // captured graph cannot be timed)
+  const bool graph = c->launch_mode == TSS_LAUNCH_GRAPH && c->prof_kind < 0;
+  r = graph ? run_verify_graph(c, seq, commit && !is_chain) : run_step(c, seq, true, commit && !is_chain);
   if (r) return r;
   c->last_M = n_nodes;
   *accept_len = c->res_host->accept_len;

@@ -33,6 +33,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -43,6 +44,7 @@ constexpr int kMaxNodes = 64;      // nodes of one verify step (u64 ancestor mas
 constexpr int kMaxLayers = 256;
 constexpr int kTileBytes = 1024;   // one packed 16 x KC weight tile
 constexpr int kAttnMaxGroups = 16; // workgroups per (head, node tile) in attention
+constexpr int kArgPages = 256;     // page ids passed in kernel arguments (contexts up to 4096 tokens)
 
 template <typename T> struct Mode;
 template <> struct Mode<__bf16> {
@@ -106,6 +108,7 @@ struct GemmArgs {
   float* q;                // [Mp][d]
   uint8_t* kv_pages;       // first page of the pool
   const int32_t* page_table;
+  int32_t pages[kArgPages];  // physical ids of the sequence's first pages (the rest: page_table)
   const float2* rope;      // [max_pos][hd/2] (cos, sin)
   int layer, n_pages_pool, n_heads, head_dim, d;
   // EPI_RESID
@@ -131,12 +134,12 @@ struct AttnArgs {
   const StepParams* sp;
   void* o;                 // [Mp][d] activation planes of the attention output
   size_t o_plane;
+  int32_t pages[kArgPages];  // physical ids of the sequence's first pages (the rest: page_table)
   float* part_o;           // [H * QT][groups][16][hd] unnormalised partial outputs
   float* part_ml;          // [H * QT][groups][16][2] (max in log2 units, sum)
   int* counters;           // [H * QT] arrivals, zero between launches
   int groups;              // workgroups per (head, node tile)
   int layer, n_pages_pool, n_heads, d, M;
-  int n_kv;
   float scale_log2;        // log2(e) / sqrt(hd)
 };
 
@@ -168,8 +171,28 @@ struct CompactArgs {
   const int32_t* page_table;
   const StepParams* sp;
   const Result* result;
-  int n_layers, n_pages_pool, n_heads, head_dim, n_kv;
+  int n_layers, n_pages_pool, n_heads, head_dim;
 };
+
+// Events bound to the next launch's own dispatch (profiling).  When `start` is
+// set, TSS_LAUNCH issues the kernel through hipExtLaunchKernel, which stamps
+// the two events with the start and end of the kernel's execution, the same
+// dispatch timestamps a kernel-trace profiler reports; otherwise it is a plain
+// launch.  Set only around direct (not captured) launches.
+struct LaunchTiming {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchTiming& launch_timing();
+
+#define TSS_LAUNCH(kernel, grid, block, lds, stream, ...)                                          \
+  do {                                                                                             \
+    const ::tss::LaunchTiming& lt_ = ::tss::launch_timing();                                       \
+    if (lt_.start)                                                                                 \
+      hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)(lds), stream, lt_.start, lt_.stop, 0u, \
+                            __VA_ARGS__);                                                          \
+    else                                                                                           \
+      hipLaunchKernelGGL(kernel, grid, block, lds, stream, __VA_ARGS__);                           \
+  } while (0)
 
 // Launchers (defined in the .hip files).  T is selected by `bf16`.
 hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_t s);
@@ -177,6 +200,8 @@ hipError_t launch_attn(bool bf16, int head_dim, int qt, const AttnArgs& a, hipSt
 hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_compact(bool bf16, const CompactArgs& a, hipStream_t s);
+const void* embed_kernel(bool bf16);  // kernel symbol, for updating a captured launch
+hipError_t init_kernel_attributes();
 hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base, hipStream_t s);
 
 // Strip width (16-row tiles per strip) of a packed matrix: gate and up tiles

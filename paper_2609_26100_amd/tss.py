@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libtss.so")
 TSS_OK, TSS_EINVAL, TSS_ENOSPACE, TSS_ECAPACITY, TSS_ESTATE, TSS_EHIP = 0, -1, -2, -3, -4, -5
 TSS_F32, TSS_BF16 = 0, 1
 TSS_COMMIT = 1
+TSS_LAUNCH_DIRECT, TSS_LAUNCH_GRAPH = 0, 1
 (TSS_K_EMBED, TSS_K_QKV, TSS_K_ATTN, TSS_K_OPROJ, TSS_K_GATEUP, TSS_K_DOWN, TSS_K_LMHEAD, TSS_K_ACCEPT,
  TSS_K_COMPACT) = range(9)
 
@@ -26,7 +27,7 @@ EXPORTS = (
     "tss_cfg_check", "tss_weights_bytes", "tss_workspace_bytes", "tss_kv_bytes", "tss_create",
     "tss_load_weights", "tss_kv_alloc", "tss_set_skip_mask", "tss_prefill", "tss_verify", "tss_get_logits",
     "tss_get_greedy", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
-    "tss_tree_meta", "tss_profile_kernel", "tss_profile_read", "tss_last_error", "tss_status_string",
+    "tss_tree_meta", "tss_set_launch_mode", "tss_profile_kernel", "tss_profile_read", "tss_last_error", "tss_status_string",
     "tss_destroy",
 )
 
@@ -76,6 +77,7 @@ def lib():
             "tss_validate_tree": (ctypes.c_int, [P, I32, I32]),
             "tss_validate_mask": (ctypes.c_int, [P, I32]),
             "tss_tree_meta": (ctypes.c_int, [P, I32, P, P]),
+            "tss_set_launch_mode": (ctypes.c_int, [P, I32]),
             "tss_profile_kernel": (ctypes.c_int, [P, I32, I32]),
             "tss_profile_read": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), I32]),
             "tss_last_error": (ctypes.c_char_p, [P]),
@@ -206,11 +208,16 @@ def tss_tree_meta(parent, n_nodes):
     return st, depth, anc
 
 
+def tss_set_launch_mode(ctx, mode):
+    _check(lib().tss_set_launch_mode(ctx, mode), ctx, "tss_set_launch_mode")
+
+
 def tss_profile_kernel(ctx, kernel, layer=-1):
     _check(lib().tss_profile_kernel(ctx, kernel, layer), ctx, "tss_profile_kernel")
 
 
 def tss_profile_read(ctx, reset=False):
+    """Returns (total_ms, count) of the profiled launches' own execution time."""
     ms, n = ctypes.c_double(), ctypes.c_int64()
     _check(lib().tss_profile_read(ctx, ctypes.byref(ms), ctypes.byref(n), int(reset)), ctx, "tss_profile_read")
     return ms.value, n.value

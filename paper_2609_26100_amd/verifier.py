@@ -40,6 +40,9 @@ class Verifier:
         for idx in range(3 + 9 * self.shape.n_layers):
             abi.tss_load_weights(self.ctx, idx, [get_tensor(idx)])
 
+    def set_launch_mode(self, mode):
+        abi.tss_set_launch_mode(self.ctx, mode)
+
     def set_mask(self, seq, mask):
         abi.tss_set_skip_mask(self.ctx, seq, mask)
 

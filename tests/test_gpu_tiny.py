@@ -223,3 +223,71 @@ def test_errors_leave_state_unchanged(pair):
     # still usable
     v.verify(0, [1, 2], commit=True)
     assert v.length(0) in (11, 12)
+
+
+def test_graph_replays_match_direct_launches(pair):
+    """Captured steps, replayed several times with eager steps in between, are
+    bit-identical to direct launches (chain, tree, two masks)."""
+    from paper_2609_26100_amd import tss as abi
+    v, m = pair
+    ctx = synth.context_tokens(SHAPE.vocab, 77, stream=50)
+    _fresh(v, m, 0, synth.mask_from_layers(L, [1]), ctx)
+    cases = [
+        (synth.context_tokens(SHAPE.vocab, 6, stream=51), None, None),
+        (synth.context_tokens(SHAPE.vocab, 9, stream=52), synth.random_tree(9, stream=53), None),
+        (synth.context_tokens(SHAPE.vocab, 3, stream=54), None, synth.mask_from_layers(L, [1, 3])),
+    ]
+    v.set_launch_mode(abi.TSS_LAUNCH_DIRECT)
+    ref = []
+    for tok, par, mask in cases:
+        ref.append((v.verify(0, tok, par, mask), v.logits(len(tok))))
+    for rep in range(3):
+        v.set_launch_mode(abi.TSS_LAUNCH_GRAPH)
+        for (tok, par, mask), (r, lg) in zip(cases, ref):
+            assert v.verify(0, tok, par, mask) == r
+            np.testing.assert_array_equal(v.logits(len(tok)), lg)
+        v.set_launch_mode(abi.TSS_LAUNCH_DIRECT)
+        assert v.verify(0, *cases[0][:2]) == ref[0][0]
+    v.set_launch_mode(abi.TSS_LAUNCH_GRAPH)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_committing_decode_loop(pair, mode):
+    """Committing steps in a row (in graph mode the same captured graph is
+    replayed at a growing context length) against the oracle doing the same
+    steps.  Each step uses a draft whose decision the oracle takes with margin;
+    when the root itself has no margin the loop moves to a fresh context."""
+    from paper_2609_26100_amd import tss as abi
+    v, m = pair
+    v.set_launch_mode(mode)
+    mask = synth.mask_from_layers(L, [2])
+    gate = 1e-3
+    steps = 0
+    for ctx_stream in range(60, 66):
+        ctx = synth.context_tokens(SHAPE.vocab, 90, stream=ctx_stream)
+        o = _fresh(v, m, 1, mask, ctx)
+        root = int(synth.context_tokens(SHAPE.vocab, 1, stream=ctx_stream + 100)[0])
+        for step in range(5):
+            g, cur = [], [root]
+            for _ in range(4):
+                g.append(int(verify(m, o, np.asarray(cur)).greedy[-1]))
+                cur.append(g[-1])
+            tok = None
+            for attempt in range(8):
+                drafts = synth.chain_draft(np.asarray(g), SHAPE.vocab, p_accept=0.7,
+                                           stream=1000 * ctx_stream + 100 * step + attempt)
+                cand = np.concatenate([[root], drafts])
+                r = verify(m, o, cand)
+                if float(r.margin[r.path].min()) > gate:
+                    tok = cand
+                    break
+            if tok is None:
+                break
+            res, (al, nt), err, compared = compare_step(SHAPE, v, 1, m, o, tok, commit=True)
+            assert compared and v.length(1) == o.n_kv
+            root = nt
+            steps += 1
+        if steps >= 6:
+            break
+    assert steps >= 6
+    v.set_launch_mode(abi.TSS_LAUNCH_GRAPH)
