@@ -91,8 +91,11 @@ enum tss_kernel {
 /* Model shape.  Constraints (checked by tss_cfg_check):
  *   d_model == n_heads * head_dim; head_dim in {64, 128};
  *   d_model and ffn_dim multiples of 32; vocab a multiple of 32;
- *   1 <= max_nodes <= 64 (nodes of one verify, root included);
- *   d_model <= 8192;
+ *   1 <= max_nodes <= 64 (nodes of one sequence in one verify, root included);
+ *   1 <= max_batch <= 8 (sequences of one tss_verify_batch);
+ *   d_model <= 8192 (<= 4096 for TSS_F32);
+ * One step carries at most min(max_nodes * max_batch, 128) rows (64 for
+ * TSS_F32): the nodes of all its sequences.
  *   dtype TSS_BF16 (bf16 weights; fp16 KV cache and attention operands; fp32
  *   activations fed to the projections as bf16 hi/lo pairs; fp32
  *   accumulation, residual stream, softmax and logits) or TSS_F32 (everything
@@ -108,7 +111,8 @@ typedef struct {
   float rope_base;     /* rotary base, 10000 for LLaMA */
   float rms_eps;       /* RMSNorm epsilon, 1e-6 */
   int32_t dtype;       /* enum tss_dtype */
-  int32_t max_nodes;   /* most nodes one tss_verify / prefill chunk may carry */
+  int32_t max_nodes;   /* most nodes of one sequence in a verify (and of a prefill chunk) */
+  int32_t max_batch;   /* most sequences of one tss_verify_batch (1 for single-sequence use) */
 } tss_model_cfg;
 
 /* Checks the constraints above.  Pure host function.  TSS_OK or TSS_EINVAL. */
@@ -168,8 +172,31 @@ int tss_prefill(tss_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n);
 int tss_verify(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent, int32_t n_nodes,
                const uint8_t* skip_mask, uint32_t flags, int32_t* accept_len, int32_t* next_token);
 
+/* Verifies several sequences in one step (the same forward as tss_verify, on
+ * the rows of every sequence at once, so each active block's weights are read
+ * once for the whole batch).
+ *   seq_ids[n_seqs]: distinct sequences.
+ *   node_offsets[n_seqs + 1]: node_offsets[0] = 0, increasing; sequence i's
+ *     nodes are draft_tokens[node_offsets[i] .. node_offsets[i + 1]), its root
+ *     first, numbered locally from 0.
+ *   tree_parents: per node the local parent index (-1 for each root), laid
+ *     out like draft_tokens; NULL = every sequence is a chain.
+ *   skip_masks: n_seqs * n_layers bytes (sequence i's mask at i * n_layers),
+ *     or NULL for each sequence's own mask.
+ * A block skipped by every sequence is not launched; inside a launched block
+ * the rows of a sequence that skips it are left untouched (no attention, no
+ * KV, residual unchanged), so each sequence's result equals its own
+ * tss_verify up to floating-point summation order.  accept_len[i] and
+ * next_token[i] are sequence i's decision; TSS_COMMIT commits every
+ * sequence.  The logits / greedy rows of tss_get_logits and tss_get_greedy
+ * follow the batch's node order. */
+int tss_verify_batch(tss_ctx* ctx, int32_t n_seqs, const int32_t* seq_ids, const int32_t* node_offsets,
+                     const int32_t* draft_tokens, const int32_t* tree_parents, const uint8_t* skip_masks,
+                     uint32_t flags, int32_t* accept_len, int32_t* next_token);
+
 /* Copies the last verify's fp32 logits [n_nodes][vocab] / greedy tokens
- * [n_nodes] to host memory.  n_nodes must not exceed the last verify's. */
+ * [n_nodes] to host memory (rows in the step's node order).  n_nodes must not
+ * exceed the last verify's node count (all sequences of a batch). */
 int tss_get_logits(tss_ctx* ctx, float* host_dst, int32_t n_nodes);
 int tss_get_greedy(tss_ctx* ctx, int32_t* host_dst, int32_t n_nodes);
 
@@ -199,6 +226,8 @@ int tss_set_launch_mode(tss_ctx* ctx, int32_t mode);
 int tss_profile_kernel(tss_ctx* ctx, int32_t kernel, int32_t layer);
 int tss_profile_read(tss_ctx* ctx, double* total_ms, int64_t* count, int32_t reset);
 
+/* Message of the context's last failure; with ctx = NULL, of the calling
+ * thread's last failed tss_create. */
 const char* tss_last_error(const tss_ctx* ctx);
 const char* tss_status_string(int status);
 void tss_destroy(tss_ctx* ctx);

@@ -53,8 +53,15 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 
   const int head = blockIdx.x, qt = blockIdx.y, g = blockIdx.z, G = gridDim.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r16 = lane & 15, grp = lane >> 4;
-  const int M = a.M, n_kv = a.sp->n_kv;
-  const int qn = qt * 16 + r16;
+  // this tile's rows and their sequence: nodes row0 .. row0 + rows - 1 are
+  // local nodes j0 .. of a sequence with Ms nodes and n_kv cached tokens
+  const int sq = a.tile_seq[qt], row0 = a.tile_row0[qt], rows = a.tile_rows[qt];
+  const int n_kv = a.sp->seq_nkv[sq];
+  const int Ms = a.sp->seq_row0[sq + 1] - a.sp->seq_row0[sq];
+  const int qn = row0 + r16;
+  const bool row_ok = r16 < rows;
+  const int32_t* pt = a.page_table + a.pt_off[sq];
+  const int arg_pages = sq == 0 ? a.n_arg_pages : 0;
 
   // B operand of S = K Q^T: lane (node qn, group grp) holds q[qn][head*HD + grp*DL + 0..DL).
   // Every wave uses the same tile, so wave 0 builds it once in LDS and the
@@ -66,7 +73,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < NQ; ++c) {
       uint4 qv = uint4{0, 0, 0, 0};
-      if (qn < M) {
+      if (row_ok) {
         if constexpr (sizeof(TK) == 2) {
           const float4 f0 = *(const float4*)(qrow + c * 8);
           const float4 f1 = *(const float4*)(qrow + c * 8 + 4);
@@ -78,8 +85,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       sm_q[lane * NQ + c] = qv;
     }
   }
-  const uint64_t anc = qn < M ? a.sp->anc[qn] : 0ull;
-  const int n_pages = (n_kv + M + kPage - 1) / kPage;
+  const uint64_t anc = row_ok ? a.sp->anc[qn] : 0ull;
+  const int n_pages = (n_kv + Ms + kPage - 1) / kPage;
 
   float m_run = -1e30f, l_run = 0.f;
   f32x4 O[NO];
@@ -88,7 +95,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 
   const size_t blk_elems = 16 * (size_t)HD;
   auto load_page = [&](int p, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
-    const int phys = p < kArgPages ? a.pages[p] : a.page_table[p];  // p is uniform across the wave
+    const int phys = p < arg_pages ? a.pages[p] : pt[p];  // p is uniform across the wave
     const TK* kb = (const TK*)a.kv_pages + (((size_t)a.layer * a.n_pages_pool + phys) * 2 * a.n_heads + head) * blk_elems;
     const TK* vb = kb + (size_t)a.n_heads * blk_elems;
     const uint4* kp = (const uint4*)(kb + r16 * HD + grp * DL);
@@ -135,7 +142,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
         vis = true;
       } else {
         const int j = slot - n_kv;
-        vis = j < M && ((anc >> j) & 1ull);
+        vis = j < Ms && ((anc >> j) & 1ull);
       }
       s[v] = vis ? S[v] * a.scale_log2 : -INFINITY;
       mloc = fmaxf(mloc, s[v]);
@@ -229,8 +236,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   for (int e = threadIdx.x; e < 64 * NO * 4; e += blockDim.x) {
     const int src = e / (NO * 4), n = (e / 4) % NO, v = e % 4;
     const int row = (src >> 4) * 4 + v;
-    const int node = qt * 16 + row;
-    if (node >= M) continue;
+    if (row >= rows) continue;
+    const int node = row0 + row;
     float num = 0.f;
     for (int w = 0; w < W; ++w) num += sm_f[w * 16 + row] * sm_o[(w * 64 + src) * OS + n * 4 + v];
     const int dim = NO * (src & 15) + n;
@@ -264,8 +271,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   const float* po0 = a.part_o + tile * G * 16 * HD;
   for (int e = threadIdx.x; e < 16 * HD; e += blockDim.x) {
     const int row = e / HD, dim = e % HD;
-    const int node = qt * 16 + row;
-    if (node >= M) continue;
+    if (row >= rows) continue;
+    const int node = row0 + row;
     float mx = -1e30f;
     for (int k = 0; k < G; ++k) mx = fmaxf(mx, pm0[k * 32 + row * 2]);
     float num = 0.f, den = 0.f;

@@ -92,6 +92,23 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Per-row data the epilogue needs (sequence, KV slot, rotary position),
+  // staged before the weight stream so its latency hides behind it.
+  __shared__ int s_seq[EPI == EPI_QKV || EPI == EPI_RESID ? kMaxRows : 1];
+  __shared__ int s_slot[EPI == EPI_QKV ? kMaxRows : 1];
+  __shared__ int s_pos[EPI == EPI_QKV ? kMaxRows : 1];
+  if constexpr (EPI == EPI_QKV || EPI == EPI_RESID) {
+    for (int r = threadIdx.x; r < M; r += blockDim.x) {
+      const int sq = a.n_seqs == 1 ? 0 : a.sp->row_seq[r];
+      s_seq[r] = sq;
+      if constexpr (EPI == EPI_QKV) {
+        const int nkv = a.sp->seq_nkv[sq];
+        s_slot[r] = nkv + r - a.sp->seq_row0[sq];  // local node j sits at slot n_kv + j
+        s_pos[r] = nkv + a.sp->depth[r];
+      }
+    }
+  }
+
   // The RMSNorm partial sums of this wave's row are loaded before the weight
   // stream (when every row has its own wave), so their latency hides behind it.
   constexpr int SSV = 8;  // parts per lane: up to 512 parts per row
@@ -187,7 +204,6 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   if constexpr (EPI == EPI_QKV) {
     const int HD = a.head_dim, d = a.d;
     const int d16 = d >> 4, hd16 = HD >> 4;
-    const int n_kv = a.sp->n_kv;
     for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
       const int row = e / COLS, col = e % COLS;
       const int n = n0 + col;
@@ -198,15 +214,16 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       float val = yfin[row * COLS + col];
       if (sec < 2) {
         const float partner = yfin[row * COLS + (col ^ 8)];
-        const float2 cs = a.rope[(size_t)a.sp->pos[row] * (HD >> 1) + 8 * t + (c & 7)];
+        const float2 cs = a.rope[(size_t)s_pos[row] * (HD >> 1) + 8 * t + (c & 7)];
         val = c < 8 ? val * cs.x - partner * cs.y : val * cs.x + partner * cs.y;
       }
       if (sec == 0) {
         a.q[(size_t)row * d + head * HD + dim] = val;
-      } else {
-        const int slot = n_kv + row;
+      } else if ((a.row_on[row >> 6] >> (row & 63)) & 1ull) {
+        const int sq = s_seq[row];
+        const int slot = s_slot[row];
         const int lp = slot >> 4;
-        const int page = lp < kArgPages ? a.pages[lp] : a.page_table[lp];
+        const int page = (sq == 0 && lp < a.n_arg_pages) ? a.pages[lp] : a.page_table[a.pt_off[sq] + lp];
         const int tin = slot & 15;
         KV* blk = (KV*)a.kv_pages +
                   ((((size_t)a.layer * a.n_pages_pool + page) * 2 + (sec - 1)) * a.n_heads + head) * (16 * (size_t)HD);
@@ -217,17 +234,21 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       }
     }
   } else if constexpr (EPI == EPI_RESID) {
+    // rows whose sequence skips this block keep h, their next-norm input and
+    // their partial sums untouched
     const int N = a.N;
     for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
       const int row = e / COLS, col = e % COLS;
+      if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
       const size_t idx = (size_t)row * N + n0 + col;
       const float hn = a.h[idx] + yfin[row * COLS + col];
       a.h[idx] = hn;
-      store_act<T>(a.xn, a.xn_plane, idx, hn * a.g_next[n0 + col]);
+      store_act<T>(a.xn, a.xn_plane, idx, hn * a.g_next[s_seq[row]][n0 + col]);
       aux[row * COLS + col] = hn * hn;
     }
     __syncthreads();
     for (int row = threadIdx.x; row < M; row += blockDim.x) {
+      if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
       float s = 0.f;
       for (int col = 0; col < COLS; ++col) s += aux[row * COLS + col];
       a.ss_out[(size_t)row * a.ss_stride + strip] = s;
@@ -260,18 +281,54 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   }
 }
 
+// dynamic LDS of the many-row variants: the CU's 160 KiB less room for the
+// kernel's static per-row arrays
+constexpr size_t kGemmLdsMax = 152 * 1024;
+
+template <int MT, int NT>
+constexpr size_t gemm_lds(int waves) {
+  return (size_t)(waves * MT * 16 * NT * 16 + MT * 16 * NT * 16 * 2 + MT * 16) * 4;
+}
+
+template <typename T, int MT, int NT, int EPI>
+static hipError_t gemm_attr() {
+  return hipFuncSetAttribute((const void*)k_gemm<T, MT, NT, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)kGemmLdsMax);
+}
+
+template <typename T, int MT>
+static hipError_t gemm_attr_mt() {
+  hipError_t e = gemm_attr<T, MT, 1, EPI_QKV>();
+  if (e == hipSuccess) e = gemm_attr<T, MT, 1, EPI_RESID>();
+  if (e == hipSuccess) e = gemm_attr<T, MT, 2, EPI_SWIGLU>();
+  if (e == hipSuccess) e = gemm_attr<T, MT, 1, EPI_LOGITS>();
+  return e;
+}
+
+// Lets the many-row variants use more than 64 KiB of LDS for the cross-wave
+// reduction (called once at context creation).
+hipError_t init_gemm_attributes() {
+  hipError_t e = gemm_attr_mt<__bf16, 5>();
+  if (e == hipSuccess) e = gemm_attr_mt<__bf16, 6>();
+  if (e == hipSuccess) e = gemm_attr_mt<__bf16, 7>();
+  if (e == hipSuccess) e = gemm_attr_mt<__bf16, 8>();
+  return e;
+}
+
 template <typename T, int MT>
 static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
   const int nt = strip_tiles(epi);
   const int strips = a.N / (16 * nt);
   const int cpw = nt == 2 ? Cpw<MT, 2>::v : Cpw<MT, 1>::v;
-  // enough waves to cover K with CPW-chunk blocks, capped by LDS (64 KiB) and 8
-  // (8-wave workgroups measured best across the 7B shapes)
+  // enough waves to cover K with CPW-chunk blocks, capped by LDS and 8
+  // (8-wave workgroups measured best across the 7B shapes); up to 64 rows the
+  // reduction stays within 64 KiB
+  const size_t cap = MT <= 4 ? 65536 : kGemmLdsMax;
   int waves = (a.nkc + cpw - 1) / cpw;
   if (waves > 8) waves = 8;
-  const int rows = MT * 16, cols = nt * 16;
-  while (waves > 1 && (size_t)(waves * rows * cols + rows * cols * 2 + rows) * 4 > 65536) waves >>= 1;
-  const size_t lds = (size_t)(waves * rows * cols + rows * cols * 2 + rows) * 4;
+  auto lds_of = [&](int w) { return nt == 2 ? gemm_lds<MT, 2>(w) : gemm_lds<MT, 1>(w); };
+  while (waves > 1 && lds_of(waves) > cap) waves >>= 1;
+  const size_t lds = lds_of(waves);
   dim3 grid(strips), block(waves * 64);
   switch (epi) {
     case EPI_QKV: TSS_LAUNCH((k_gemm<T, MT, 1, EPI_QKV>), grid, block, lds, s, a); break;
@@ -282,18 +339,29 @@ static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <typename T>
-static hipError_t launch_t(int epi, int mt, const GemmArgs& a, hipStream_t s) {
-  switch (mt) {
-    case 1: return launch_mt<T, 1>(epi, a, s);
-    case 2: return launch_mt<T, 2>(epi, a, s);
-    case 3: return launch_mt<T, 3>(epi, a, s);
-    default: return launch_mt<T, 4>(epi, a, s);
-  }
-}
-
+// mt = 16-row tiles of the step's rows: up to 8 (128 rows) in the bf16 mode,
+// up to 4 (64 rows) in the f32 mode.
 hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_t s) {
-  return bf16 ? launch_t<__bf16>(epi, mt, a, s) : launch_t<float>(epi, mt, a, s);
+  if (bf16) {
+    switch (mt) {
+      case 1: return launch_mt<__bf16, 1>(epi, a, s);
+      case 2: return launch_mt<__bf16, 2>(epi, a, s);
+      case 3: return launch_mt<__bf16, 3>(epi, a, s);
+      case 4: return launch_mt<__bf16, 4>(epi, a, s);
+      case 5: return launch_mt<__bf16, 5>(epi, a, s);
+      case 6: return launch_mt<__bf16, 6>(epi, a, s);
+      case 7: return launch_mt<__bf16, 7>(epi, a, s);
+      case 8: return launch_mt<__bf16, 8>(epi, a, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  switch (mt) {
+    case 1: return launch_mt<float, 1>(epi, a, s);
+    case 2: return launch_mt<float, 2>(epi, a, s);
+    case 3: return launch_mt<float, 3>(epi, a, s);
+    case 4: return launch_mt<float, 4>(epi, a, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace tss

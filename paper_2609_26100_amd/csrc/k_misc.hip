@@ -5,17 +5,19 @@
 
 namespace tss {
 
-// h[m] = E[tok[m]] (fp32); xn[m] = h[m] * gain (activation planes) for the
-// first RMSNorm the rows meet; ss_out[m] = sum h[m]^2 (one partial,
-// fixed-order reduction).  Each thread gathers up to four 16-byte chunks of
-// the row, issued together.  The step's parameters arrive by value and
-// workgroup 0 stores them for the later kernels of the step (this replaces a
-// separate host-to-device copy, which costs as much as a kernel launch).
+// h[m] = E[tok[m]] (fp32); xn[m] = h[m] * gain (activation planes) with the
+// gain of the first RMSNorm the row's sequence meets; ss_out[m][p] = sum of
+// h[m][k]^2 over the 16 columns of part p (the format every projection
+// epilogue writes, so each norm reads d/16 parts whatever produced them).
+// Each thread gathers up to four 16-byte chunks of the row, issued together.
+// The step's parameters arrive by value and workgroup 0 stores them for the
+// later kernels of the step (this replaces a separate host-to-device copy,
+// which costs as much as a kernel launch).
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
   constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   constexpr int MAXC = 4;                 // chunks per thread (d <= 4 * 256 * E)
-  __shared__ float red[256];
+  __shared__ float rowv[4 * 256 * 8];
   const int m = blockIdx.x;
   const int d = a.d, nch = d / E;
   if (m == 0) {
@@ -23,6 +25,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     uint32_t* dst = (uint32_t*)a.sp_dev;
     for (int i = threadIdx.x; i < (int)(sizeof(StepParams) / 4); i += 256) dst[i] = src[i];
   }
+  const float* gain = a.gain[a.sp.row_seq[m]];
   const T* row = (const T*)a.embed + (size_t)a.sp.tok[m] * d;
   uint4 raw[MAXC];
 #pragma unroll
@@ -30,7 +33,6 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     const int c = threadIdx.x + i * 256;
     raw[i] = c < nch ? ((const uint4*)row)[c] : uint4{0, 0, 0, 0};
   }
-  float s = 0.f;
 #pragma unroll
   for (int i = 0; i < MAXC; ++i) {
     const int c = threadIdx.x + i * 256;
@@ -41,17 +43,17 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
       const int k = c * E + j;
       const float v = (float)e[j];
       a.h[(size_t)m * d + k] = v;
-      store_act<T>(a.xn, a.xn_plane, (size_t)m * d + k, v * a.gain[k]);
-      s += v * v;
+      store_act<T>(a.xn, a.xn_plane, (size_t)m * d + k, v * gain[k]);
+      rowv[k] = v;
     }
   }
-  red[threadIdx.x] = s;
   __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
-    __syncthreads();
+  for (int p = threadIdx.x; p < d / 16; p += 256) {
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) s += rowv[p * 16 + k] * rowv[p * 16 + k];
+    a.ss_out[(size_t)m * a.ss_stride + p] = s;
   }
-  if (threadIdx.x == 0) a.ss_out[(size_t)m * a.ss_stride] = red[0];
 }
 
 // (value, index) order of the greedy argmax: larger value first, lower index on ties.
@@ -59,17 +61,19 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
-// One workgroup of 16 waves.  Greedy token per node from the lm_head's
-// per-strip partials (each node gets 16 / M waves, loads issued eight at a
-// time), then the accept scan over the tree: a node is accepted when its
-// parent is and its token equals the parent's greedy token; the deepest
-// accepted node (lowest id among equal depths) gives accept_len and the bonus
-// token.
+// One workgroup of 16 waves.  Greedy token per row from the lm_head's
+// per-strip partials (each row gets 16 / M waves, loads issued eight at a
+// time), then one accept scan per sequence over its tree: a node is accepted
+// when its parent is and its token equals the parent's greedy token; the
+// deepest accepted node (lowest id among equal depths) gives accept_len and
+// the bonus token.
 __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a) {
-  __shared__ int32_t g[kMaxNodes];
+  __shared__ int32_t g[kMaxRows];
   __shared__ float bvs[16];
   __shared__ int32_t bis[16];
-  __shared__ int32_t s_tok[kMaxNodes], s_par[kMaxNodes], s_dep[kMaxNodes];
+  __shared__ int32_t s_tok[kMaxRows];
+  __shared__ int8_t s_par[kMaxRows];
+  __shared__ uint8_t s_dep[kMaxRows];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int M = a.M;
   if (threadIdx.x < M) {
@@ -77,7 +81,7 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a) {
     s_par[threadIdx.x] = a.sp->parent[threadIdx.x];
     s_dep[threadIdx.x] = a.sp->depth[threadIdx.x];
   }
-  const int wpr = M >= 16 ? 1 : (M >= 8 ? 2 : (M >= 4 ? 4 : (M >= 2 ? 8 : 16)));  // waves per node
+  const int wpr = M >= 16 ? 1 : (M >= 8 ? 2 : (M >= 4 ? 4 : (M >= 2 ? 8 : 16)));  // waves per row
   const int groups = 16 / wpr;
   const int grp_id = wave / wpr, sub = wave % wpr;
   for (int m0 = 0; m0 < M; m0 += groups) {
@@ -119,61 +123,67 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a) {
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) {
-    uint64_t acc = 1ull;  // bit i: node i accepted
+  const int sq = threadIdx.x;
+  if (sq < a.sp->n_seqs) {
+    const int r0 = a.sp->seq_row0[sq], n = a.sp->seq_row0[sq + 1] - r0;
+    const int32_t* gs = g + r0;
+    uint64_t acc = 1ull;  // bit i: local node i accepted
     int best = 0;
-    for (int i = 1; i < M; ++i) {
-      const int p = s_par[i];
-      if (((acc >> p) & 1ull) && s_tok[i] == g[p]) {
+    for (int i = 1; i < n; ++i) {
+      const int p = s_par[r0 + i];
+      if (((acc >> p) & 1ull) && s_tok[r0 + i] == gs[p]) {
         acc |= 1ull << i;
-        if (s_dep[i] > s_dep[best]) best = i;
+        if (s_dep[r0 + i] > s_dep[r0 + best]) best = i;
       }
     }
-    const int len = s_dep[best];
+    const int len = s_dep[r0 + best];
     for (int copy = 0; copy < 2; ++copy) {
-      Result* r = copy == 0 ? a.result : a.result_host;
+      Result* r = (copy == 0 ? a.result : a.result_host) + sq;
       r->accept_len = len;
-      r->next_token = g[best];
+      r->next_token = gs[best];
       r->best = best;
       r->path_len = len + 1;
       for (int j = best, dd = len; dd >= 0; --dd) {
         r->path[dd] = j;
-        j = dd > 0 ? s_par[j] : 0;
+        j = dd > 0 ? s_par[r0 + j] : 0;
       }
     }
   }
 }
 
-// Moves the K/V of the accepted tree path (nodes path[1..a]) to the slots
-// right after the context (n_kv + 1 .. n_kv + a), for the layers that ran.
-// Every source slot n_kv + path[d] has path[d] >= d, so reading all sources
-// before writing any destination is enough; one thread owns one dimension.
-// T = KV element type.
+// Moves the K/V of an accepted tree path (local nodes path[1..a]) to the
+// slots right after the context (n_kv + 1 .. n_kv + a), for the layers its
+// sequence ran.  Every source slot n_kv + path[d] has path[d] >= d, so
+// reading all sources before writing any destination is enough; one thread
+// owns one dimension.  grid = (layer, head, listed sequence); T = KV type.
 template <typename T>
 __global__ __launch_bounds__(128) void k_compact(CompactArgs a) {
-  const int layer = blockIdx.x, head = blockIdx.y, dim = threadIdx.x;
-  if (a.sp->mask[layer] || dim >= a.head_dim) return;
-  const int n_kv = a.sp->n_kv;
-  const int len = a.result->accept_len;
+  const int layer = blockIdx.x, head = blockIdx.y, z = blockIdx.z, dim = threadIdx.x;
+  if (!((a.lay_on[z][layer >> 6] >> (layer & 63)) & 1ull) || dim >= a.head_dim) return;
+  const int sq = a.seq[z];
+  const int n_kv = a.sp->seq_nkv[sq];
+  const Result& res = a.result[sq];
+  const int len = res.accept_len;
   const int HD = a.head_dim;
+  const int32_t* pt = a.page_table + a.pt_off[z];
   T kbuf[kMaxNodes], vbuf[kMaxNodes];
   auto kaddr = [&](int slot) {
-    const int page = a.page_table[slot >> 4], tin = slot & 15;
+    const int page = pt[slot >> 4], tin = slot & 15;
     T* blk = (T*)a.kv_pages + ((((size_t)layer * a.n_pages_pool + page) * 2 + 0) * a.n_heads + head) * (16 * (size_t)HD);
     return blk + tin * HD + dim;
   };
   auto vaddr = [&](int slot) {
-    const int page = a.page_table[slot >> 4], tin = slot & 15;
+    const int page = pt[slot >> 4], tin = slot & 15;
     T* blk = (T*)a.kv_pages + ((((size_t)layer * a.n_pages_pool + page) * 2 + 1) * a.n_heads + head) * (16 * (size_t)HD);
     return blk + (tin >> 2) * HD * 4 + dim * 4 + (tin & 3);
   };
   for (int d = 1; d <= len; ++d) {
-    const int src = n_kv + a.result->path[d];
+    const int src = n_kv + res.path[d];
     kbuf[d] = *kaddr(src);
     vbuf[d] = *vaddr(src);
   }
   for (int d = 1; d <= len; ++d) {
-    if (a.result->path[d] == d) continue;
+    if (res.path[d] == d) continue;
     *kaddr(n_kv + d) = kbuf[d];
     *vaddr(n_kv + d) = vbuf[d];
   }
@@ -207,11 +217,11 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_compact(bool bf16, const CompactArgs& a, hipStream_t s) {
+hipError_t launch_compact(bool bf16, int n_seqs, const CompactArgs& a, hipStream_t s) {
   if (bf16)
-    TSS_LAUNCH(k_compact<_Float16>, dim3(a.n_layers, a.n_heads), dim3(128), 0, s, a);
+    TSS_LAUNCH(k_compact<_Float16>, dim3(a.n_layers, a.n_heads, n_seqs), dim3(128), 0, s, a);
   else
-    TSS_LAUNCH(k_compact<float>, dim3(a.n_layers, a.n_heads), dim3(128), 0, s, a);
+    TSS_LAUNCH(k_compact<float>, dim3(a.n_layers, a.n_heads, n_seqs), dim3(128), 0, s, a);
   return hipGetLastError();
 }
 

@@ -53,6 +53,13 @@ int elem_size(const tss_model_cfg* c) { return c->dtype == TSS_BF16 ? 2 : 4; }
 // activation planes: two bf16 planes (hi, lo) in the bf16 mode, one fp32 plane otherwise
 int act_planes(const tss_model_cfg* c) { return c->dtype == TSS_BF16 ? 2 : 1; }
 int round16(int x) { return (x + 15) & ~15; }
+// rows one step can carry: the nodes of every sequence of a batch (the GEMMs
+// take up to 8 sixteen-row tiles in the bf16 mode, 4 in the f32 mode)
+int row_cap(const tss_model_cfg* c) {
+  return std::min(c->max_nodes * c->max_batch, c->dtype == TSS_BF16 ? kMaxRows : 64);
+}
+// 16-row attention tiles one step can carry (tiles never straddle sequences)
+int tile_cap(const tss_model_cfg* c) { return std::min(kMaxTiles, (row_cap(c) + 15 * c->max_batch) / 16); }
 
 int cfg_ok(const tss_model_cfg* c) {
   if (!c) return 0;
@@ -63,6 +70,8 @@ int cfg_ok(const tss_model_cfg* c) {
   if (c->d_model > 8192) return 0;  // RMSNorm partial sums: at most 512 per row
   if (c->dtype != TSS_F32 && c->dtype != TSS_BF16) return 0;
   if (c->max_nodes < 1 || c->max_nodes > kMaxNodes) return 0;
+  if (c->max_batch < 1 || c->max_batch > kMaxBatch) return 0;
+  if (c->dtype == TSS_F32 && c->d_model > 4096) return 0;  // embedding gather: 4 chunks of 4 per thread
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return 0;
   return 1;
 }
@@ -91,12 +100,12 @@ WeightLayout weight_layout(const tss_model_cfg* c) {
 WsLayout ws_layout(const tss_model_cfg* c) {
   WsLayout w;
   const size_t es = elem_size(c), d = c->d_model, f = c->ffn_dim, v = c->vocab;
-  const size_t Mp = round16(c->max_nodes);
+  const size_t Mp = round16(row_cap(c));
   const size_t ap = act_planes(c);
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return o; };
   w.sp = take(sizeof(StepParams));
-  w.result = take(sizeof(Result));
+  w.result = take(kMaxBatch * sizeof(Result));
   w.h = take(Mp * d * 4);
   w.xa = take(ap * Mp * d * es);
   w.xm = take(ap * Mp * d * es);
@@ -105,7 +114,7 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   w.q = take(Mp * d * 4);
   w.o = take(ap * Mp * d * es);
   w.act = take(ap * Mp * f * es);
-  const size_t tiles = (size_t)c->n_heads * (Mp / 16);
+  const size_t tiles = (size_t)c->n_heads * tile_cap(c);
   w.part_o = take(tiles * kAttnMaxGroups * 16 * c->head_dim * 4);
   w.part_ml = take(tiles * kAttnMaxGroups * 16 * 2 * 4);
   w.counters = take(tiles * 4);
@@ -160,7 +169,15 @@ struct tss_ctx {
   hipEvent_t stage_ev[2] = {nullptr, nullptr};
   int stage_cur = 0;
   StepParams* sp_host = nullptr;
-  Result* res_host = nullptr;     // host-mapped, written by the accept kernel
+  // the step being enqueued: its sequences, their masks (n_seqs x n_layers)
+  // and which of them need their accepted tree path moved after the commit
+  struct Step {
+    int n_seqs = 0;
+    int32_t seq[kMaxBatch] = {};
+    bool compact[kMaxBatch] = {};
+    std::vector<uint8_t> mask;
+  } step;
+  Result* res_host = nullptr;     // [kMaxBatch] host-mapped, written by the accept kernel
   Result* res_dev_map = nullptr;  // its device address
   int last_M = 0;
   bool poisoned = false;
@@ -188,6 +205,12 @@ struct tss_ctx {
 };
 
 namespace {
+
+// message of the last failed tss_create on this thread (tss_last_error(NULL))
+std::string& create_error() {
+  static thread_local std::string e = "null context";
+  return e;
+}
 
 int fail(tss_ctx* c, int code, const std::string& msg) {
   if (c) c->err = msg;
@@ -319,10 +342,11 @@ const char* tss_status_string(int s) {
   }
 }
 
-const char* tss_last_error(const tss_ctx* c) { return c ? c->err.c_str() : "null context"; }
+const char* tss_last_error(const tss_ctx* c) { return c ? c->err.c_str() : create_error().c_str(); }
 
 int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, size_t weights_bytes,
                void* dev_workspace, size_t workspace_bytes, tss_ctx** out) {
+  create_error() = "null context";
   if (!out) return TSS_EINVAL;
   *out = nullptr;
   if (!cfg_ok(cfg) || !dev_weights || !dev_workspace) return TSS_EINVAL;
@@ -332,23 +356,34 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
   c->bf16 = cfg->dtype == TSS_BF16;
   c->es = elem_size(cfg);
   c->KC = 64 / c->es;
-  c->Mp = round16(cfg->max_nodes);
+  c->Mp = round16(row_cap(cfg));
   c->stream = (hipStream_t)hip_stream;
   c->w = (uint8_t*)dev_weights;
   c->ws = (uint8_t*)dev_workspace;
   c->wl = weight_layout(cfg);
   c->wsl = ws_layout(cfg);
+  const char* where = "pinned step parameters";
   hipError_t e = hipHostMalloc((void**)&c->sp_host, sizeof(StepParams), hipHostMallocDefault);
+  auto step = [&](const char* w, hipError_t r) {
+    if (e == hipSuccess) {
+      where = w;
+      e = r;
+    }
+  };
   if (e == hipSuccess)
-    e = hipHostMalloc((void**)&c->res_host, sizeof(Result), hipHostMallocMapped | hipHostMallocCoherent);
-  if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&c->res_dev_map, c->res_host, 0);
-  if (e == hipSuccess) e = hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * (c->Mp / 16) * 4,
-                                          c->stream);
-  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
-  if (e == hipSuccess) e = init_kernel_attributes();
-  if (e == hipSuccess) e = hipEventCreate(&c->ev0);
-  if (e == hipSuccess) e = hipEventCreate(&c->ev1);
+    step("mapped result buffer",
+         hipHostMalloc((void**)&c->res_host, kMaxBatch * sizeof(Result), hipHostMallocMapped | hipHostMallocCoherent));
+  if (e == hipSuccess) step("mapped result address", hipHostGetDevicePointer((void**)&c->res_dev_map, c->res_host, 0));
+  if (e == hipSuccess)
+    step("attention counters",
+         hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * tile_cap(cfg) * 4, c->stream));
+  if (e == hipSuccess) step("stream sync", hipStreamSynchronize(c->stream));
+  if (e == hipSuccess) step("attention LDS attribute", init_kernel_attributes());
+  if (e == hipSuccess) step("projection LDS attribute", init_gemm_attributes());
+  if (e == hipSuccess) step("timing event", hipEventCreate(&c->ev0));
+  if (e == hipSuccess) step("timing event", hipEventCreate(&c->ev1));
   if (e != hipSuccess) {
+    create_error() = std::string("tss_create: ") + where + ": " + hipGetErrorString(e);
     tss_destroy(c);
     return TSS_EHIP;
   }
@@ -604,32 +639,60 @@ int attn_groups_for(int n_kv, int M) {
   return std::max(1, std::min(kAttnMaxGroups, (n_pages + 15) / 16));
 }
 
-// Enqueues embed, the active blocks and (for verify) lm_head + accept for the
-// nodes in c->sp_host on stream s.  seq's page table is used for KV.  Every
+// Attention workgroups per (head, tile) of the step: sized for its longest
+// sequence (context + nodes).
+int step_attn_groups(const tss_ctx* c) {
+  const StepParams& sp = *c->sp_host;
+  int g = 1;
+  for (int i = 0; i < sp.n_seqs; ++i)
+    g = std::max(g, attn_groups_for(sp.seq_nkv[i], sp.seq_row0[i + 1] - sp.seq_row0[i]));
+  return g;
+}
+
+// Layer after `l` that sequence i runs (n_layers = none), and the gain of the
+// RMSNorm that layer (or the final norm) applies first.
+int next_active(const tss_ctx* c, int i, int l) {
+  const int L = c->cfg.n_layers;
+  const uint8_t* m = c->step.mask.data() + (size_t)i * L;
+  for (int k = l + 1; k < L; ++k)
+    if (!m[k]) return k;
+  return L;
+}
+const float* attn_gain_of(const tss_ctx* c, int layer) {
+  return (const float*)(c->w + (layer < c->cfg.n_layers ? c->wl.layers[layer].attn_norm : c->wl.final_norm));
+}
+
+// Enqueues embed, the blocks that any sequence of the step runs and (for
+// verify) lm_head + accept (+ KV compaction) for the rows in c->sp_host and
+// the sequences in c->step, on stream s.  A block that every sequence skips
+// is not launched; inside a launched block the rows of sequences that skip it
+// are left untouched (their attention tiles are not even listed).  Every
 // kernel argument except the embedding kernel's step parameters depends only
-// on (seq, mask, node count, tree/chain, attention groups), so a captured
-// sequence can be replayed for later steps of the same shape.
-int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) {
+// on the step's shape (sequences, masks, node counts, compaction, attention
+// groups), so a captured sequence of launches can be replayed for later steps
+// of the same shape.
+int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
   const tss_model_cfg& cf = c->cfg;
   const StepParams& sp = *c->sp_host;
+  const tss_ctx::Step& st = c->step;
   const int M = sp.M, L = cf.n_layers, d = cf.d_model, f = cf.ffn_dim, H = cf.n_heads, hd = cf.head_dim;
+  const int B = st.n_seqs;
   const int mt = (M + 15) / 16;
   uint8_t* ws = c->ws;
   StepParams* sp_dev = (StepParams*)(ws + c->wsl.sp);
-  const int32_t* pt = (const int32_t*)(c->kv + c->kvl.page_table) + (size_t)seq * c->kvl.pages_per_seq;
-  const int32_t* pt_h = c->pt_host.data() + (size_t)seq * c->kvl.pages_per_seq;
+  const int pps = c->kvl.pages_per_seq;
+  const int32_t* pt_all = (const int32_t*)(c->kv + c->kvl.page_table);
   uint8_t* pages = c->kv + c->kvl.pages;
   const float2* rope = (const float2*)(c->kv + c->kvl.rope);
   c->cur_stream = s;
-
-  std::vector<int> active;
-  for (int l = 0; l < L; ++l)
-    if (!sp.mask[l]) active.push_back(l);
-  auto attn_gain = [&](int idx) -> const float* {
-    return (const float*)(c->w + (idx < (int)active.size() ? c->wl.layers[active[idx]].attn_norm : c->wl.final_norm));
-  };
-
   c->prof_armed = false;
+
+  int32_t pt_off[kMaxBatch] = {};
+  for (int i = 0; i < B; ++i) pt_off[i] = st.seq[i] * pps;
+  // a single sequence's first page ids travel in the kernel arguments
+  int32_t arg_pages[kArgPages] = {};
+  const int n_arg_pages = B == 1 ? std::min(pps, kArgPages) : 0;
+  for (int i = 0; i < n_arg_pages; ++i) arg_pages[i] = c->pt_host[(size_t)pt_off[0] + i];
 
   {
     const EmbedArgs a = embed_args(c);
@@ -641,23 +704,42 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
   GemmArgs base{};
   base.M = M;
   base.Mp = c->Mp;
+  base.n_seqs = B;
   const bool two = act_planes(&cf) == 2;
   const size_t plane_d = two ? (size_t)c->Mp * d : 0, plane_f = two ? (size_t)c->Mp * f : 0;
   base.eps = cf.rms_eps;
   base.norm_dim = d;
   base.ss_stride = d / 16;
+  base.ss_nparts = d / 16;
   base.am_stride = cf.vocab / 16;
   base.sp = sp_dev;
+  base.row_on[0] = base.row_on[1] = ~0ull;
 
-  // attention: one page per wave where possible, at most kAttnMaxGroups
-  // sixteen-wave workgroups per (head, node tile)
-  const int attn_groups = attn_groups_for(sp.n_kv, M);
+  const int attn_groups = step_attn_groups(c);
 
-  for (size_t idx = 0; idx < active.size(); ++idx) {
-    const int l = active[idx];
+  for (int l = 0; l < L; ++l) {
+    // rows and attention tiles of the sequences that run block l
+    uint64_t row_on[kMaxRows / 64] = {0, 0};
+    AttnArgs at{};
+    int n_tiles = 0;
+    for (int i = 0; i < B; ++i) {
+      if (st.mask[(size_t)i * L + l]) continue;
+      const int r0 = sp.seq_row0[i], r1 = sp.seq_row0[i + 1];
+      for (int r = r0; r < r1; ++r) row_on[r >> 6] |= 1ull << (r & 63);
+      for (int t0 = r0; t0 < r1; t0 += 16) {
+        at.tile_row0[n_tiles] = (int16_t)t0;
+        at.tile_rows[n_tiles] = (uint8_t)std::min(16, r1 - t0);
+        at.tile_seq[n_tiles] = (uint8_t)i;
+        ++n_tiles;
+      }
+    }
+    if (n_tiles == 0) continue;  // every sequence skips this block
     const LayerW& W = c->wl.layers[l];
+    GemmArgs lb = base;
+    lb.row_on[0] = row_on[0];
+    lb.row_on[1] = row_on[1];
     {  // RMSNorm + QKV + RoPE + KV append
-      GemmArgs a = base;
+      GemmArgs a = lb;
       a.w = c->w + W.qkv;
       a.x = ws + c->wsl.xa;
       a.x_plane = plane_d;
@@ -665,11 +747,12 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       a.N = 3 * d;
       a.nkc = d / c->KC;
       a.ss_in = (const float*)(ws + c->wsl.ss_a);
-      a.ss_nparts = idx == 0 ? 1 : d / 16;
       a.q = (float*)(ws + c->wsl.q);
       a.kv_pages = pages;
-      a.page_table = pt;
-      for (int i = 0; i < kArgPages; ++i) a.pages[i] = i < c->kvl.pages_per_seq ? pt_h[i] : 0;
+      a.page_table = pt_all;
+      std::memcpy(a.pt_off, pt_off, sizeof(pt_off));
+      a.n_arg_pages = n_arg_pages;
+      std::memcpy(a.pages, arg_pages, sizeof(arg_pages));
       a.rope = rope;
       a.layer = l;
       a.n_pages_pool = c->kvl.n_pages;
@@ -681,14 +764,16 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       ps.done();
     }
     {  // tree attention
-      AttnArgs a{};
+      AttnArgs& a = at;
       a.q = (const float*)(ws + c->wsl.q);
       a.kv_pages = pages;
-      a.page_table = pt;
+      a.page_table = pt_all;
       a.sp = sp_dev;
       a.o = ws + c->wsl.o;
       a.o_plane = plane_d;
-      for (int i = 0; i < kArgPages; ++i) a.pages[i] = i < c->kvl.pages_per_seq ? pt_h[i] : 0;
+      std::memcpy(a.pt_off, pt_off, sizeof(pt_off));
+      a.n_arg_pages = n_arg_pages;
+      std::memcpy(a.pages, arg_pages, sizeof(arg_pages));
       a.part_o = (float*)(ws + c->wsl.part_o);
       a.part_ml = (float*)(ws + c->wsl.part_ml);
       a.counters = (int*)(ws + c->wsl.counters);
@@ -697,14 +782,13 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       a.n_pages_pool = c->kvl.n_pages;
       a.n_heads = H;
       a.d = d;
-      a.M = M;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
       ProfScope ps(c, TSS_K_ATTN, l);
-      HIPCHK(launch_attn(c->bf16, hd, mt, a, s), "attention");
+      HIPCHK(launch_attn(c->bf16, hd, n_tiles, a, s), "attention");
       ps.done();
     }
-    {  // O projection + residual; next norm input
-      GemmArgs a = base;
+    {  // O projection + residual; next norm input (this block's MLP norm)
+      GemmArgs a = lb;
       a.w = c->w + W.o;
       a.x = ws + c->wsl.o;
       a.x_plane = plane_d;
@@ -714,14 +798,14 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       a.h = (float*)(ws + c->wsl.h);
       a.xn = ws + c->wsl.xm;
       a.xn_plane = plane_d;
-      a.g_next = (const float*)(c->w + W.mlp_norm);
+      for (int i = 0; i < kMaxBatch; ++i) a.g_next[i] = (const float*)(c->w + W.mlp_norm);
       a.ss_out = (float*)(ws + c->wsl.ss_m);
       ProfScope ps(c, TSS_K_OPROJ, l);
       HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, a, s), "o gemm");
       ps.done();
     }
     {  // RMSNorm + gate/up + SwiGLU
-      GemmArgs a = base;
+      GemmArgs a = lb;
       a.w = c->w + W.gateup;
       a.x = ws + c->wsl.xm;
       a.x_plane = plane_d;
@@ -729,15 +813,14 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       a.N = 2 * f;
       a.nkc = d / c->KC;
       a.ss_in = (const float*)(ws + c->wsl.ss_m);
-      a.ss_nparts = d / 16;
       a.act = ws + c->wsl.act;
       a.act_plane = plane_f;
       ProfScope ps(c, TSS_K_GATEUP, l);
       HIPCHK(launch_gemm(c->bf16, EPI_SWIGLU, mt, a, s), "gate/up gemm");
       ps.done();
     }
-    {  // down projection + residual; next norm input
-      GemmArgs a = base;
+    {  // down projection + residual; next norm input (each sequence's next block, or the final norm)
+      GemmArgs a = lb;
       a.w = c->w + W.down;
       a.x = ws + c->wsl.act;
       a.x_plane = plane_f;
@@ -747,7 +830,7 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       a.h = (float*)(ws + c->wsl.h);
       a.xn = ws + c->wsl.xa;
       a.xn_plane = plane_d;
-      a.g_next = attn_gain((int)idx + 1);
+      for (int i = 0; i < kMaxBatch; ++i) a.g_next[i] = attn_gain_of(c, i < B ? next_active(c, i, l) : L);
       a.ss_out = (float*)(ws + c->wsl.ss_a);
       ProfScope ps(c, TSS_K_DOWN, l);
       HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, a, s), "down gemm");
@@ -765,7 +848,6 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       a.N = cf.vocab;
       a.nkc = d / c->KC;
       a.ss_in = (const float*)(ws + c->wsl.ss_a);
-      a.ss_nparts = active.empty() ? 1 : d / 16;
       a.logits = (float*)(ws + c->wsl.logits);
       a.am_val = (float*)(ws + c->wsl.am_val);
       a.am_idx = (int32_t*)(ws + c->wsl.am_idx);
@@ -788,10 +870,19 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       HIPCHK(launch_accept(a, s), "accept");
       ps.done();
     }
-    if (compact) {
-      CompactArgs a{};
+    CompactArgs a{};
+    int nz = 0;
+    for (int i = 0; i < B; ++i) {
+      if (!st.compact[i]) continue;
+      a.seq[nz] = i;
+      a.pt_off[nz] = pt_off[i];
+      for (int l = 0; l < L; ++l)
+        if (!st.mask[(size_t)i * L + l]) a.lay_on[nz][l >> 6] |= 1ull << (l & 63);
+      ++nz;
+    }
+    if (nz > 0) {
       a.kv_pages = pages;
-      a.page_table = pt;
+      a.page_table = pt_all;
       a.sp = sp_dev;
       a.result = (const Result*)(ws + c->wsl.result);
       a.n_layers = L;
@@ -799,7 +890,7 @@ int enqueue_step(tss_ctx* c, int seq, bool verify, bool compact, hipStream_t s) 
       a.n_heads = H;
       a.head_dim = hd;
       ProfScope ps(c, TSS_K_COMPACT, -1);
-      HIPCHK(launch_compact(c->bf16, a, s), "kv compaction");
+      HIPCHK(launch_compact(c->bf16, nz, a, s), "kv compaction");
       ps.done();
     }
   }
@@ -819,8 +910,8 @@ int finish_step(tss_ctx* c) {
   return TSS_OK;
 }
 
-int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
-  const int r = enqueue_step(c, seq, verify, compact, c->stream);
+int run_step(tss_ctx* c, bool verify) {
+  const int r = enqueue_step(c, verify, c->stream);
   if (r) return r;
   return finish_step(c);
 }
@@ -830,14 +921,11 @@ int run_step(tss_ctx* c, int seq, bool verify, bool compact) {
 EmbedArgs embed_args(tss_ctx* c) {
   const tss_model_cfg& cf = c->cfg;
   const StepParams& sp = *c->sp_host;
-  int first = -1;
-  for (int l = 0; l < cf.n_layers && first < 0; ++l)
-    if (!sp.mask[l]) first = l;
   EmbedArgs a{};
   a.embed = c->w + c->wl.embed;
   a.sp = sp;
   a.sp_dev = (StepParams*)(c->ws + c->wsl.sp);
-  a.gain = (const float*)(c->w + (first >= 0 ? c->wl.layers[first].attn_norm : c->wl.final_norm));
+  for (int i = 0; i < kMaxBatch; ++i) a.gain[i] = attn_gain_of(c, i < c->step.n_seqs ? next_active(c, i, -1) : 0);
   a.h = (float*)(c->ws + c->wsl.h);
   a.xn = c->ws + c->wsl.xa;
   a.xn_plane = act_planes(&cf) == 2 ? (size_t)c->Mp * cf.d_model : 0;
@@ -850,16 +938,20 @@ EmbedArgs embed_args(tss_ctx* c) {
 
 // A verify step from the graph cache: captured on first use of its shape,
 // then replayed with the embedding kernel's step parameters updated.
-int run_verify_graph(tss_ctx* c, int seq, bool compact) {
+int run_verify_graph(tss_ctx* c) {
   const StepParams& sp = *c->sp_host;
+  const tss_ctx::Step& st = c->step;
   std::string key;
-  key.reserve(64 + c->cfg.n_layers);
+  key.reserve(64 + st.mask.size());
   auto put = [&](int v) { key.append((const char*)&v, sizeof(v)); };
-  put(seq);
-  put(sp.M);
-  put(compact);
-  put(attn_groups_for(sp.n_kv, sp.M));
-  key.append((const char*)sp.mask, c->cfg.n_layers);
+  put(st.n_seqs);
+  for (int i = 0; i < st.n_seqs; ++i) {
+    put(st.seq[i]);
+    put(sp.seq_row0[i + 1] - sp.seq_row0[i]);
+    put(st.compact[i]);
+  }
+  put(step_attn_groups(c));
+  key.append((const char*)st.mask.data(), st.mask.size());
   tss_ctx::GraphEntry* g = nullptr;
   for (auto& e : c->graphs)
     if (e.key == key) g = &e;
@@ -878,7 +970,7 @@ int run_verify_graph(tss_ctx* c, int seq, bool compact) {
     e.key = key;
     c->prof_armed = false;
     HIPCHK(hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal), "begin capture");
-    const int r = enqueue_step(c, seq, true, compact, c->cap_stream);
+    const int r = enqueue_step(c, true, c->cap_stream);
     hipGraph_t graph = nullptr;
     const hipError_t ce = hipStreamEndCapture(c->cap_stream, &graph);
     if (r) {
@@ -932,6 +1024,95 @@ int check_ready(tss_ctx* c, int seq) {
   return TSS_OK;
 }
 
+// The verify of a batch of sequences (tss_verify is a batch of one).  Every
+// check runs before anything is enqueued; sequence state changes only after
+// the step succeeded.
+int verify_batch(tss_ctx* c, int32_t n_seqs, const int32_t* seq_ids, const int32_t* node_offsets,
+                 const int32_t* tokens, const int32_t* parents, const uint8_t* masks, uint32_t flags,
+                 int32_t* accept_len, int32_t* next_token) {
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  if (!c->kv) return fail(c, TSS_ESTATE, "no KV pool bound (tss_kv_alloc)");
+  if (n_seqs < 1 || n_seqs > c->cfg.max_batch) return fail(c, TSS_EINVAL, "n_seqs outside [1, max_batch]");
+  if (!seq_ids || !node_offsets || !tokens || !accept_len || !next_token) return fail(c, TSS_EINVAL, "null argument");
+  if (flags & ~(uint32_t)TSS_COMMIT) return fail(c, TSS_EINVAL, "unknown flag");
+  const int L = c->cfg.n_layers;
+  if (node_offsets[0] != 0) return fail(c, TSS_EINVAL, "node_offsets[0] must be 0");
+  for (int i = 0; i < n_seqs; ++i) {
+    const int sq = seq_ids[i];
+    if (sq < 0 || sq >= c->n_seqs) return fail(c, TSS_EINVAL, "unknown sequence");
+    for (int j = 0; j < i; ++j)
+      if (seq_ids[j] == sq) return fail(c, TSS_EINVAL, "a sequence appears twice in one batch");
+    const int n = node_offsets[i + 1] - node_offsets[i];
+    if (validate_tree(parents ? parents + node_offsets[i] : nullptr, n, c->cfg.max_nodes) != TSS_OK)
+      return fail(c, TSS_EINVAL, "invalid draft tree (n_nodes, parent[0] = -1, 0 <= parent[i] < i)");
+  }
+  const int M = node_offsets[n_seqs];
+  if (M > row_cap(&c->cfg))
+    return fail(c, TSS_EINVAL, "the batch's nodes exceed the step's row capacity");
+  if (masks && !mask_ok(masks, n_seqs * L)) return fail(c, TSS_EINVAL, "mask bytes must be 0 or 1");
+  for (int r = 0; r < M; ++r)
+    if (tokens[r] < 0 || tokens[r] >= c->cfg.vocab) return fail(c, TSS_EINVAL, "token outside [0, vocab)");
+  for (int i = 0; i < n_seqs; ++i) {
+    const int sq = seq_ids[i];
+    const int n = node_offsets[i + 1] - node_offsets[i];
+    if (c->n_kv[sq] + n > c->max_tokens) return fail(c, TSS_ECAPACITY, "verify exceeds the sequence's KV capacity");
+    const uint8_t* m = masks ? masks + (size_t)i * L : c->mask[sq].data();
+    for (int l = 0; l < L; ++l)
+      if (!m[l] && c->kv_len[sq][l] != c->n_kv[sq])
+        return fail(c, TSS_ESTATE, "an active layer lacks K/V for the committed context");
+  }
+
+  const bool commit = flags & TSS_COMMIT;
+  StepParams& sp = *c->sp_host;
+  std::memset(&sp, 0, sizeof(sp));
+  tss_ctx::Step& st = c->step;
+  st.n_seqs = n_seqs;
+  st.mask.resize((size_t)n_seqs * L);
+  sp.M = M;
+  sp.n_seqs = n_seqs;
+  for (int i = 0; i < n_seqs; ++i) {
+    const int sq = seq_ids[i], r0 = node_offsets[i], n = node_offsets[i + 1] - r0;
+    st.seq[i] = sq;
+    std::memcpy(st.mask.data() + (size_t)i * L, masks ? masks + (size_t)i * L : c->mask[sq].data(), L);
+    sp.seq_row0[i] = r0;
+    sp.seq_nkv[i] = c->n_kv[sq];
+    int32_t depth[kMaxNodes];
+    uint64_t anc[kMaxNodes];
+    const int32_t* par = parents ? parents + r0 : nullptr;
+    tree_meta(par, n, depth, anc);
+    bool chain = true;
+    for (int j = 0; j < n; ++j) {
+      const int p = par ? par[j] : j - 1;
+      if (j > 0 && p != j - 1) chain = false;
+      sp.tok[r0 + j] = tokens[r0 + j];
+      sp.parent[r0 + j] = (int8_t)p;
+      sp.depth[r0 + j] = (uint8_t)depth[j];
+      sp.anc[r0 + j] = anc[j];
+      sp.row_seq[r0 + j] = (uint8_t)i;
+    }
+    st.compact[i] = commit && !chain;
+  }
+  sp.seq_row0[n_seqs] = M;
+  // event timing of one launch needs direct launches (events recorded inside a
+  // captured graph cannot be timed)
+  const bool graph = c->launch_mode == TSS_LAUNCH_GRAPH && c->prof_kind < 0;
+  const int r = graph ? run_verify_graph(c) : run_step(c, true);
+  if (r) return r;
+  c->last_M = M;
+  for (int i = 0; i < n_seqs; ++i) {
+    const int sq = seq_ids[i];
+    accept_len[i] = c->res_host[i].accept_len;
+    next_token[i] = c->res_host[i].next_token;
+    if (commit) {
+      c->n_kv[sq] += c->res_host[i].accept_len + 1;
+      const uint8_t* m = st.mask.data() + (size_t)i * L;
+      for (int l = 0; l < L; ++l)
+        if (!m[l]) c->kv_len[sq][l] = c->n_kv[sq];
+    }
+  }
+  return TSS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -948,26 +1129,31 @@ int tss_prefill(tss_ctx* c, int32_t seq, const int32_t* tokens, int32_t n) {
   for (int l = 0; l < L; ++l)
     if (!c->mask[seq][l] && c->kv_len[seq][l] != c->n_kv[seq])
       return fail(c, TSS_ESTATE, "an active layer lacks K/V for the committed context");
-  const int chunk = std::min(c->cfg.max_nodes, kMaxNodes);
+  const int chunk = std::min({c->cfg.max_nodes, kMaxNodes, row_cap(&c->cfg)});
+  tss_ctx::Step& st = c->step;
+  st.n_seqs = 1;
+  st.seq[0] = seq;
+  st.compact[0] = false;
+  st.mask.assign(c->mask[seq].begin(), c->mask[seq].end());
   for (int done = 0; done < n; done += chunk) {
     const int M = std::min(chunk, n - done);
     StepParams& sp = *c->sp_host;
     std::memset(&sp, 0, sizeof(sp));
     sp.M = M;
-    sp.n_kv = c->n_kv[seq];
+    sp.n_seqs = 1;
+    sp.seq_row0[1] = M;
+    sp.seq_nkv[0] = c->n_kv[seq];
     for (int i = 0; i < M; ++i) {
       sp.tok[i] = tokens[done + i];
-      sp.parent[i] = i - 1;
-      sp.depth[i] = i;
-      sp.pos[i] = sp.n_kv + i;
+      sp.parent[i] = (int8_t)(i - 1);
+      sp.depth[i] = (uint8_t)i;
       sp.anc[i] = (i == 63) ? ~0ull : ((1ull << (i + 1)) - 1);
     }
-    for (int l = 0; l < L; ++l) sp.mask[l] = c->mask[seq][l];
-    r = run_step(c, seq, false, false);
+    r = run_step(c, false);
     if (r) return r;
     c->n_kv[seq] += M;
     for (int l = 0; l < L; ++l)
-      if (!sp.mask[l]) c->kv_len[seq][l] = c->n_kv[seq];
+      if (!c->mask[seq][l]) c->kv_len[seq][l] = c->n_kv[seq];
   }
   return TSS_OK;
 }
@@ -975,52 +1161,18 @@ int tss_prefill(tss_ctx* c, int32_t seq, const int32_t* tokens, int32_t n) {
 int tss_verify(tss_ctx* c, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent, int32_t n_nodes,
                const uint8_t* skip_mask, uint32_t flags, int32_t* accept_len, int32_t* next_token) {
   if (!c) return TSS_EINVAL;
-  int r = check_ready(c, seq);
+  const int r = check_ready(c, seq);
   if (r) return r;
-  if (!draft_tokens || !accept_len || !next_token) return fail(c, TSS_EINVAL, "null argument");
-  if (flags & ~(uint32_t)TSS_COMMIT) return fail(c, TSS_EINVAL, "unknown flag");
-  if (validate_tree(tree_parent, n_nodes, c->cfg.max_nodes) != TSS_OK)
-    return fail(c, TSS_EINVAL, "invalid draft tree (n_nodes, parent[0] = -1, 0 <= parent[i] < i)");
-  const int L = c->cfg.n_layers;
-  if (skip_mask && !mask_ok(skip_mask, L)) return fail(c, TSS_EINVAL, "mask bytes must be 0 or 1");
-  for (int i = 0; i < n_nodes; ++i)
-    if (draft_tokens[i] < 0 || draft_tokens[i] >= c->cfg.vocab) return fail(c, TSS_EINVAL, "token outside [0, vocab)");
-  const int n_kv = c->n_kv[seq];
-  if (n_kv + n_nodes > c->max_tokens) return fail(c, TSS_ECAPACITY, "verify exceeds the sequence's KV capacity");
-  const uint8_t* m = skip_mask ? skip_mask : c->mask[seq].data();
-  for (int l = 0; l < L; ++l)
-    if (!m[l] && c->kv_len[seq][l] != n_kv)
-      return fail(c, TSS_ESTATE, "an active layer lacks K/V for the committed context");
+  const int32_t offs[2] = {0, n_nodes};
+  return verify_batch(c, 1, &seq, offs, draft_tokens, tree_parent, skip_mask, flags, accept_len, next_token);
+}
 
-  StepParams& sp = *c->sp_host;
-  std::memset(&sp, 0, sizeof(sp));
-  sp.M = n_nodes;
-  sp.n_kv = n_kv;
-  tree_meta(tree_parent, n_nodes, sp.depth, sp.anc);
-  for (int i = 0; i < n_nodes; ++i) {
-    sp.tok[i] = draft_tokens[i];
-    sp.parent[i] = tree_parent ? tree_parent[i] : i - 1;
-    sp.pos[i] = n_kv + sp.depth[i];
-  }
-  for (int l = 0; l < L; ++l) sp.mask[l] = m[l];
-  const bool commit = flags & TSS_COMMIT;
-  bool is_chain = true;
-  for (int i = 1; i < n_nodes; ++i)
-    if (sp.parent[i] != i - 1) is_chain = false;
-  // event timing of one launch needs direct launches (events recorded inside a
-  // captured graph cannot be timed)
-  const bool graph = c->launch_mode == TSS_LAUNCH_GRAPH && c->prof_kind < 0;
-  r = graph ? run_verify_graph(c, seq, commit && !is_chain) : run_step(c, seq, true, commit && !is_chain);
-  if (r) return r;
-  c->last_M = n_nodes;
-  *accept_len = c->res_host->accept_len;
-  *next_token = c->res_host->next_token;
-  if (commit) {
-    c->n_kv[seq] = n_kv + c->res_host->accept_len + 1;
-    for (int l = 0; l < L; ++l)
-      if (!m[l]) c->kv_len[seq][l] = c->n_kv[seq];
-  }
-  return TSS_OK;
+int tss_verify_batch(tss_ctx* c, int32_t n_seqs, const int32_t* seq_ids, const int32_t* node_offsets,
+                     const int32_t* draft_tokens, const int32_t* tree_parents, const uint8_t* skip_masks,
+                     uint32_t flags, int32_t* accept_len, int32_t* next_token) {
+  if (!c) return TSS_EINVAL;
+  return verify_batch(c, n_seqs, seq_ids, node_offsets, draft_tokens, tree_parents, skip_masks, flags, accept_len,
+                      next_token);
 }
 
 int tss_get_logits(tss_ctx* c, float* host_dst, int32_t n_nodes) {

@@ -40,11 +40,14 @@
 namespace tss {
 
 constexpr int kPage = 16;          // tokens per KV page
-constexpr int kMaxNodes = 64;      // nodes of one verify step (u64 ancestor masks)
+constexpr int kMaxNodes = 64;      // nodes of one sequence in one step (u64 ancestor masks)
+constexpr int kMaxBatch = 8;       // sequences of one step
+constexpr int kMaxRows = 128;      // rows (nodes of every sequence) of one step
+constexpr int kMaxTiles = 16;      // 16-row attention tiles of one step (per-sequence tiles)
 constexpr int kMaxLayers = 256;
 constexpr int kTileBytes = 1024;   // one packed 16 x KC weight tile
 constexpr int kAttnMaxGroups = 16; // workgroups per (head, node tile) in attention
-constexpr int kArgPages = 256;     // page ids passed in kernel arguments (contexts up to 4096 tokens)
+constexpr int kArgPages = 256;     // page ids passed in kernel arguments (one sequence, up to 4096 tokens)
 
 template <typename T> struct Mode;
 template <> struct Mode<__bf16> {
@@ -68,23 +71,32 @@ __device__ __forceinline__ void store_act(void* base, size_t plane, size_t idx, 
   }
 }
 
+// Per-step data that changes from step to step (tokens, tree, context
+// lengths).  Rows are the nodes of every sequence of the step, sequence after
+// sequence; a sequence's nodes are numbered locally from 0 (its root).
 struct StepParams {
-  int32_t M;                       // nodes in this step
-  int32_t n_kv;                    // committed context length
-  int32_t tok[kMaxNodes];
-  int32_t pos[kMaxNodes];          // n_kv + depth
-  int32_t parent[kMaxNodes];
-  int32_t depth[kMaxNodes];
-  uint64_t anc[kMaxNodes];         // bit j: node j is this node or an ancestor
-  uint8_t mask[kMaxLayers];        // 1 = block skipped in this step
+  int32_t M;                       // rows
+  int32_t n_seqs;
+  int32_t seq_row0[kMaxBatch + 1]; // first row of each sequence; seq_row0[n_seqs] = M
+  int32_t seq_nkv[kMaxBatch];      // committed context length of each sequence
+  int32_t tok[kMaxRows];
+  uint64_t anc[kMaxRows];          // bit j: local node j is this node or one of its ancestors
+  int8_t parent[kMaxRows];         // local parent (-1 for the root)
+  uint8_t depth[kMaxRows];
+  uint8_t row_seq[kMaxRows];       // sequence (0 .. n_seqs-1) of the row
 };
+
+// Position of a row: its sequence's committed length plus its depth.
+__device__ __forceinline__ int row_pos(const StepParams* sp, int row) {
+  return sp->seq_nkv[sp->row_seq[row]] + sp->depth[row];
+}
 
 struct Result {
   int32_t accept_len;
   int32_t next_token;
   int32_t best;
   int32_t path_len;                // accept_len + 1
-  int32_t path[kMaxNodes];         // node ids root -> best
+  int32_t path[kMaxNodes];         // local node ids root -> best
 };
 
 enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
@@ -104,18 +116,24 @@ struct GemmArgs {
   float eps;
   int Mp;                  // row stride of the partial-sum arrays
   const StepParams* sp;
+  // rows whose sequence runs this block (bit r of row_on[r / 64]); the QKV
+  // and residual epilogues write nothing for the other rows
+  uint64_t row_on[kMaxRows / 64];
+  int n_seqs;
   // EPI_QKV
   float* q;                // [Mp][d]
   uint8_t* kv_pages;       // first page of the pool
-  const int32_t* page_table;
-  int32_t pages[kArgPages];  // physical ids of the sequence's first pages (the rest: page_table)
+  const int32_t* page_table;  // the pool's page table; sequence s's pages start at pt_off[s]
+  int32_t pt_off[kMaxBatch];
+  int32_t n_arg_pages;     // with one sequence: valid entries of pages[]
+  int32_t pages[kArgPages];  // physical ids of the first pages of a single sequence
   const float2* rope;      // [max_pos][hd/2] (cos, sin)
   int layer, n_pages_pool, n_heads, head_dim, d;
   // EPI_RESID
   float* h;                // [Mp][N] residual, updated in place
   void* xn;                // [Mp][N] activation planes of h_new * g_next
   size_t xn_plane;
-  const float* g_next;     // gain of the next RMSNorm
+  const float* g_next[kMaxBatch];  // gain of each sequence's next RMSNorm
   float* ss_out;           // [M][ss_stride] partial sums of h_new^2, one per strip
   // EPI_SWIGLU
   void* act;               // [Mp][N/2] activation planes of silu(gate) * up
@@ -134,24 +152,31 @@ struct AttnArgs {
   const StepParams* sp;
   void* o;                 // [Mp][d] activation planes of the attention output
   size_t o_plane;
-  int32_t pages[kArgPages];  // physical ids of the sequence's first pages (the rest: page_table)
-  float* part_o;           // [H * QT][groups][16][hd] unnormalised partial outputs
-  float* part_ml;          // [H * QT][groups][16][2] (max in log2 units, sum)
-  int* counters;           // [H * QT] arrivals, zero between launches
+  float* part_o;           // [H * kMaxTiles][groups][16][hd] unnormalised partial outputs
+  float* part_ml;          // [H * kMaxTiles][groups][16][2] (max in log2 units, sum)
+  int* counters;           // [H * kMaxTiles] arrivals, zero between launches
   int groups;              // workgroups per (head, node tile)
-  int layer, n_pages_pool, n_heads, d, M;
+  int layer, n_pages_pool, n_heads, d;
   float scale_log2;        // log2(e) / sqrt(hd)
+  // node tiles of the sequences that run this block: tile t covers rows
+  // tile_row0[t] .. + tile_rows[t] - 1, all of sequence tile_seq[t]
+  int16_t tile_row0[kMaxTiles];
+  uint8_t tile_rows[kMaxTiles];
+  uint8_t tile_seq[kMaxTiles];
+  int32_t pt_off[kMaxBatch];
+  int32_t n_arg_pages;     // with one sequence: valid entries of pages[]
+  int32_t pages[kArgPages];  // physical ids of the first pages of a single sequence
 };
 
 struct EmbedArgs {
   const void* embed;       // [V][d] T
   StepParams sp;           // this step's parameters (by value) ...
   StepParams* sp_dev;      // ... copied here for the later kernels of the step
-  const float* gain;       // gain of the first RMSNorm the rows meet
+  const float* gain[kMaxBatch];  // per sequence: gain of the first RMSNorm its rows meet
   float* h;                // [Mp][d]
   void* xn;                // [Mp][d] activation planes
   size_t xn_plane;
-  float* ss_out;           // [M][ss_stride], part 0
+  float* ss_out;           // [M][ss_stride]: sums of h^2 over 16-column parts
   int ss_stride;
   int d, M;
 };
@@ -162,16 +187,21 @@ struct AcceptArgs {
   int nparts, M, am_stride;
   const StepParams* sp;
   int32_t* greedy;         // [Mp]
-  Result* result;          // device copy (read by the compaction kernel)
-  Result* result_host;     // host-mapped pinned copy (read by the host after the step)
+  Result* result;          // [n_seqs] device copy (read by the compaction kernel)
+  Result* result_host;     // [n_seqs] host-mapped pinned copy (read by the host after the step)
 };
 
 struct CompactArgs {
   uint8_t* kv_pages;
   const int32_t* page_table;
   const StepParams* sp;
-  const Result* result;
+  const Result* result;    // [n_seqs]
   int n_layers, n_pages_pool, n_heads, head_dim;
+  // grid.z walks the sequences listed here (those whose accepted tree path
+  // needs moving); lay_on[i] has bit l set for each layer sequence seq[i] ran
+  int32_t seq[kMaxBatch];
+  int32_t pt_off[kMaxBatch];
+  uint64_t lay_on[kMaxBatch][kMaxLayers / 64];
 };
 
 // Events bound to the next launch's own dispatch (profiling).  When `start` is
@@ -199,9 +229,10 @@ hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_
 hipError_t launch_attn(bool bf16, int head_dim, int qt, const AttnArgs& a, hipStream_t s);
 hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
-hipError_t launch_compact(bool bf16, const CompactArgs& a, hipStream_t s);
+hipError_t launch_compact(bool bf16, int n_seqs, const CompactArgs& a, hipStream_t s);
 const void* embed_kernel(bool bf16);  // kernel symbol, for updating a captured launch
-hipError_t init_kernel_attributes();
+hipError_t init_kernel_attributes();  // attention
+hipError_t init_gemm_attributes();
 hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base, hipStream_t s);
 
 // Strip width (16-row tiles per strip) of a packed matrix: gate and up tiles

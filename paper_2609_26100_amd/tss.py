@@ -26,7 +26,7 @@ TSS_LAUNCH_DIRECT, TSS_LAUNCH_GRAPH = 0, 1
 EXPORTS = (
     "tss_cfg_check", "tss_weights_bytes", "tss_workspace_bytes", "tss_kv_bytes", "tss_create",
     "tss_load_weights", "tss_kv_alloc", "tss_set_skip_mask", "tss_prefill", "tss_verify", "tss_get_logits",
-    "tss_get_greedy", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
+    "tss_verify_batch", "tss_get_greedy", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
     "tss_tree_meta", "tss_set_launch_mode", "tss_profile_kernel", "tss_profile_read", "tss_last_error", "tss_status_string",
     "tss_destroy",
 )
@@ -37,7 +37,7 @@ class tss_model_cfg(ctypes.Structure):
         ("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
         ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32), ("vocab", ctypes.c_int32),
         ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float), ("dtype", ctypes.c_int32),
-        ("max_nodes", ctypes.c_int32),
+        ("max_nodes", ctypes.c_int32), ("max_batch", ctypes.c_int32),
     ]
 
 
@@ -70,6 +70,7 @@ def lib():
             "tss_set_skip_mask": (ctypes.c_int, [P, I32, P]),
             "tss_prefill": (ctypes.c_int, [P, I32, P, I32]),
             "tss_verify": (ctypes.c_int, [P, I32, P, P, I32, P, U32, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
+            "tss_verify_batch": (ctypes.c_int, [P, I32, P, P, P, P, P, U32, P, P]),
             "tss_get_logits": (ctypes.c_int, [P, P, I32]),
             "tss_get_greedy": (ctypes.c_int, [P, P, I32]),
             "tss_seq_length": (ctypes.c_int, [P, I32, ctypes.POINTER(I32)]),
@@ -107,9 +108,10 @@ def _check(status, ctx=None, what=""):
         raise TSSError(status, f"{what}: {msg}")
 
 
-def make_cfg(shape, max_nodes=64) -> tss_model_cfg:
+def make_cfg(shape, max_nodes=64, max_batch=1) -> tss_model_cfg:
     return tss_model_cfg(shape.n_layers, shape.d_model, shape.n_heads, shape.head_dim, shape.ffn_dim, shape.vocab,
-                         shape.rope_base, shape.rms_eps, TSS_BF16 if shape.dtype == "bf16" else TSS_F32, max_nodes)
+                         shape.rope_base, shape.rms_eps, TSS_BF16 if shape.dtype == "bf16" else TSS_F32, max_nodes,
+                         max_batch)
 
 
 def tss_cfg_check(cfg) -> int:
@@ -132,7 +134,8 @@ def tss_create(cfg, hip_stream, dev_weights, weights_bytes, dev_workspace, works
     out = ctypes.c_void_p()
     st = lib().tss_create(ctypes.byref(cfg), hip_stream, dev_weights, weights_bytes, dev_workspace, workspace_bytes,
                           ctypes.byref(out))
-    _check(st, None, "tss_create")
+    if st != TSS_OK:
+        raise TSSError(st, f"tss_create: {lib().tss_last_error(None).decode()}")
     return out.value
 
 
@@ -166,6 +169,25 @@ def tss_verify(ctx, seq, draft_tokens, tree_parent=None, skip_mask=None, flags=0
     _check(lib().tss_verify(ctx, seq, _ptr(t), _ptr(p), len(t), _ptr(m), flags, ctypes.byref(al), ctypes.byref(nt)),
            ctx, "tss_verify")
     return al.value, nt.value
+
+
+def tss_verify_batch(ctx, seq_ids, draft_tokens, node_offsets, tree_parents=None, skip_masks=None, flags=0):
+    """Returns (accept_len[n_seqs], next_token[n_seqs])."""
+    ids = np.ascontiguousarray(seq_ids, dtype=np.int32)
+    offs = np.ascontiguousarray(node_offsets, dtype=np.int32)
+    t = np.ascontiguousarray(draft_tokens, dtype=np.int32)
+    p = None if tree_parents is None else np.ascontiguousarray(tree_parents, dtype=np.int32)
+    m = None if skip_masks is None else np.ascontiguousarray(skip_masks, dtype=np.uint8)
+    n = len(ids)
+    if len(offs) != n + 1 or (p is not None and len(p) != len(t)) or (m is not None and m.size % max(n, 1)):
+        raise ValueError("seq_ids, node_offsets, tree_parents and skip_masks do not describe one batch")
+    if len(offs) and offs[-1] != len(t):
+        raise ValueError("node_offsets[-1] must equal the number of draft tokens")
+    al = np.zeros(n, dtype=np.int32)
+    nt = np.zeros(n, dtype=np.int32)
+    _check(lib().tss_verify_batch(ctx, n, _ptr(ids), _ptr(offs), _ptr(t), _ptr(p), _ptr(m), flags, _ptr(al), _ptr(nt)),
+           ctx, "tss_verify_batch")
+    return al, nt
 
 
 def tss_get_logits(ctx, n_nodes, vocab):

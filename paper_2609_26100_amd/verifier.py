@@ -12,13 +12,13 @@ from . import tss as abi
 
 class Verifier:
     def __init__(self, shape, n_seqs=1, max_tokens=2048, max_nodes=64, device="cuda:0", stream=None,
-                 page_order=None):
+                 page_order=None, max_batch=1):
         import torch
 
         self.torch = torch
         self.shape = shape
         self.device = torch.device(device)
-        self.cfg = abi.make_cfg(shape, max_nodes)
+        self.cfg = abi.make_cfg(shape, max_nodes, max_batch)
         if abi.tss_cfg_check(self.cfg) != abi.TSS_OK:
             raise ValueError(f"unsupported shape {shape}")
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
@@ -33,6 +33,7 @@ class Verifier:
                                   self.workspace.data_ptr(), sb)
         abi.tss_kv_alloc(self.ctx, n_seqs, max_tokens, self.kv_pool.data_ptr(), kb, page_order)
         self.n_seqs, self.max_tokens = n_seqs, max_tokens
+        self._mask = {i: np.zeros(shape.n_layers, np.uint8) for i in range(n_seqs)}
 
     def load(self, get_tensor):
         """Streams every tensor, in the ABI's tensor order, from get_tensor(index) -> host array in the
@@ -45,12 +46,34 @@ class Verifier:
 
     def set_mask(self, seq, mask):
         abi.tss_set_skip_mask(self.ctx, seq, mask)
+        L = self.shape.n_layers
+        self._mask[seq] = np.zeros(L, np.uint8) if mask is None else np.asarray(mask, dtype=np.uint8).copy()
 
     def prefill(self, seq, tokens):
         abi.tss_prefill(self.ctx, seq, tokens)
 
     def verify(self, seq, tokens, parent=None, mask=None, commit=False):
         return abi.tss_verify(self.ctx, seq, tokens, parent, mask, abi.TSS_COMMIT if commit else 0)
+
+    def verify_batch(self, seqs, drafts, parents=None, masks=None, commit=False):
+        """drafts: one token array per sequence (root first); parents: None or one parent array (or None for
+        a chain) per sequence; masks: None or one mask (or None for the sequence's own) per sequence.
+        Returns (accept_len[n], next_token[n])."""
+        offs = np.concatenate([[0], np.cumsum([len(t) for t in drafts])]).astype(np.int32)
+        tokens = np.concatenate([np.asarray(t, dtype=np.int32) for t in drafts])
+        par = None
+        if parents is not None and any(p is not None for p in parents):
+            par = np.concatenate([np.arange(-1, len(t) - 1, dtype=np.int32) if p is None else np.asarray(p, np.int32)
+                                  for t, p in zip(drafts, parents)])
+        m = None
+        if masks is not None:
+            L = self.shape.n_layers
+            rows = []
+            for sq, mk in zip(seqs, masks):
+                rows.append(self._mask[sq] if mk is None else np.asarray(mk, dtype=np.uint8))
+            m = np.concatenate(rows).astype(np.uint8)
+            assert m.size == L * len(seqs)
+        return abi.tss_verify_batch(self.ctx, seqs, tokens, offs, par, m, abi.TSS_COMMIT if commit else 0)
 
     def logits(self, n_nodes):
         return abi.tss_get_logits(self.ctx, n_nodes, self.shape.vocab)

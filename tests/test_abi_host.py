@@ -52,12 +52,25 @@ def test_7b_sizes():
 
 @pytest.mark.parametrize("field,val", [("head_dim", 96), ("d_model", 4000), ("vocab", 32001), ("max_nodes", 65),
                                        ("max_nodes", 0), ("n_layers", 0), ("dtype", 7), ("rms_eps", 0.0),
-                                       ("ffn_dim", 11000), ("n_layers", 257)])
+                                       ("ffn_dim", 11000), ("n_layers", 257), ("max_batch", 0), ("max_batch", 9)])
 def test_cfg_rejects(field, val):
     cfg = abi.make_cfg(synth.LLAMA_7B)
     setattr(cfg, field, val)
     assert abi.tss_cfg_check(cfg) == abi.TSS_EINVAL
     assert abi.tss_weights_bytes(cfg) == 0
+
+
+def test_cfg_batch_capacity():
+    """The workspace holds the rows of a whole batch (up to 128 bf16 / 64 fp32 rows)."""
+    one = abi.make_cfg(synth.LLAMA_13B, max_nodes=9, max_batch=1)
+    eight = abi.make_cfg(synth.LLAMA_13B, max_nodes=9, max_batch=8)
+    assert abi.tss_cfg_check(eight) == abi.TSS_OK
+    assert abi.tss_workspace_bytes(eight) > abi.tss_workspace_bytes(one)
+    big = abi.make_cfg(synth.LLAMA_13B, max_nodes=64, max_batch=8)   # capped at 128 rows
+    assert abi.tss_workspace_bytes(big) < 2 * abi.tss_workspace_bytes(abi.make_cfg(synth.LLAMA_13B, 64, 2))
+    wide = abi.make_cfg(synth.TINY)
+    wide.d_model, wide.n_heads = 8192, 128     # fp32 embedding gather covers d <= 4096
+    assert abi.tss_cfg_check(wide) == abi.TSS_EINVAL
 
 
 def test_validate_tree():
@@ -116,6 +129,7 @@ def test_null_context_calls_fail_cleanly():
     al, nt = ctypes.c_int32(), ctypes.c_int32()
     assert L.tss_verify(None, 0, None, None, 1, None, 0, ctypes.byref(al), ctypes.byref(nt)) == abi.TSS_EINVAL
     assert L.tss_prefill(None, 0, None, 0) == abi.TSS_EINVAL
+    assert L.tss_verify_batch(None, 1, None, None, None, None, None, 0, None, None) == abi.TSS_EINVAL
     assert L.tss_set_skip_mask(None, 0, None) == abi.TSS_EINVAL
     assert L.tss_load_weights(None, 0, 1, None) == abi.TSS_EINVAL
     L.tss_destroy(None)
