@@ -47,6 +47,23 @@ def algorithmic_bytes(shape, active, n_ctx, M):
     return active * per_layer + 2 * v * d + 2 * M * d + 2 * d + 4 * M * v
 
 
+def batch_bytes(shape, seqs):
+    """Algorithmic bytes of one step over several sequences, each given as
+    (skip mask, context length, nodes): the weights and norm gains of every
+    block some sequence runs (read once for the batch), each sequence's KV read
+    and write for the blocks it runs, lm_head, embedding rows, final norm and
+    the logits of all rows."""
+    d, f, v = shape.d_model, shape.ffn_dim, shape.vocab
+    union = np.zeros(shape.n_layers, bool)
+    kv = 0
+    for mask, n_ctx, m in seqs:
+        act = np.asarray(mask) == 0
+        union |= act
+        kv += int(act.sum()) * (4 * d * n_ctx + 4 * d * m)
+    M = sum(m for _, _, m in seqs)
+    return int(union.sum()) * (2 * (4 * d * d + 3 * d * f) + 4 * d) + kv + 2 * v * d + 2 * M * d + 2 * d + 4 * M * v
+
+
 def gateup_bytes(shape, M):
     """Algorithmic bytes of one gate/up launch: W_gate and W_up (bf16), the
     normalised input rows, the SwiGLU output rows."""
@@ -62,7 +79,8 @@ def run_gpu(args):
     shape = synth.LLAMA_7B
     M = K_DRAFT + 1
     t0 = time.time()
-    v = Verifier(shape, n_seqs=1, max_tokens=CTX + 64, max_nodes=64, device="cuda:0")
+    # room for the 2048-token tree workload, which reuses these weights
+    v = Verifier(shape, n_seqs=1, max_tokens=2048 + 64, max_nodes=64, device="cuda:0")
     gen = synth.abi_tensor_loader(shape)
     t_gen = [0.0]
 
@@ -160,8 +178,186 @@ def run_gpu(args):
     for s in args.skips[1:]:
         results[s]["latency_ratio_vs_dense"] = results[s]["latency_us_median"] / d0["latency_us_median"]
         results[s]["byte_ratio_vs_dense"] = results[s]["algorithmic_GB"] / d0["algorithmic_GB"]
+    return shape, results, prof, v
+
+
+def _load_verifier(shape, **kw):
+    from paper_2609_26100_amd.verifier import Verifier
+    t0 = time.time()
+    v = Verifier(shape, device="cuda:0", **kw)
+    gen = synth.abi_tensor_loader(shape)
+    n = 3 + 9 * shape.n_layers
+
+    def get(idx):
+        if idx and idx % 90 == 0:
+            log(f"{shape.name}: tensor {idx}/{n} ({time.time() - t0:.0f}s)")
+        return gen(idx)
+    v.load(get)
+    log(f"{shape.name}: weights generated and loaded in {time.time() - t0:.1f}s")
+    return v
+
+
+def _free(v):
+    import torch
     v.close()
-    return shape, results, prof
+    del v.weights, v.workspace, v.kv_pool
+    torch.cuda.empty_cache()
+
+
+def _timed(step, n_warmup, n_steps):
+    """Blocking steps; returns per-step latency (s) and per-step accepted tokens."""
+    for _ in range(n_warmup):
+        step(0)
+    lat, acc = np.empty(n_steps), np.empty(n_steps)
+    for i in range(n_steps):
+        a = time.perf_counter()
+        acc[i] = step(i)
+        lat[i] = time.perf_counter() - a
+    return lat, acc
+
+
+def _summary(lat, acc, by):
+    med = float(np.median(lat))
+    return {"latency_us_median": med * 1e6, "latency_us_p10": float(np.percentile(lat, 10)) * 1e6,
+            "latency_us_p90": float(np.percentile(lat, 90)) * 1e6, "accepted_tok_s": float(acc.sum() / lat.sum()),
+            "mean_accepted_per_step": float(acc.mean()), "algorithmic_GB": by / 1e9,
+            "roofline_latency_us": by / PEAK_HBM * 1e6, "roofline_frac": by / PEAK_HBM / med, "steps": len(lat)}
+
+
+def workload_tree_7b(args, v=None):
+    """7B, 2048-token context, 60-node top-k-style tree (depth 6, branching
+    4,3,2,2,1,1, level quotas 4,12,20,12,8,4), 6 layers skipped from 16-31;
+    the greedy token sits in a random child slot with probability 0.6."""
+    shape = synth.LLAMA_7B
+    ctx_n = 2048
+    if v is None:
+        v = _load_verifier(shape, n_seqs=1, max_tokens=ctx_n + 64, max_nodes=64)
+    v.truncate(0, 0)
+    mask = synth.random_skip_mask(shape.n_layers, 16, 31, 6, stream=3)
+    toks = synth.context_tokens(shape.vocab, ctx_n + 1, stream=3)
+    v.set_mask(0, mask)
+    v.prefill(0, toks[:ctx_n])
+    parent = synth.topk_tree_parents((4, 3, 2, 2, 1, 1), (4, 12, 20, 12, 8, 4))
+
+    def greedy_of(tok, node):
+        path = [node]
+        while parent[path[-1]] >= 0:
+            path.append(int(parent[path[-1]]))
+        chain = tok[path[::-1]]
+        v.verify(0, chain)
+        return int(v.greedy(len(chain))[-1])
+    tokens = synth.tree_draft_tokens(parent, int(toks[ctx_n]), greedy_of, shape.vocab, 0.6, stream=3)
+
+    def step(i):
+        al, _ = v.verify(0, tokens, parent, commit=True)
+        v.truncate(0, ctx_n)
+        return al + 1
+    lat, acc = _timed(step, args.warmup, args.aux_steps)
+    out = _summary(lat, acc, batch_bytes(shape, [(mask, ctx_n, len(parent))]))
+    out.update({"workload": "7B-shape, 60-node draft tree + root, 2048-token context, 6 layers skipped",
+                "skipped_layers": np.nonzero(mask)[0].tolist(), "nodes": len(parent)})
+    _free(v)
+    return out
+
+
+def workload_batch_13b(args):
+    """13B, 8 sequences with contexts U{512..4096}, chain k=8 (p=0.6 on each
+    sequence's masked greedy continuation), per-sequence masks of U{0..10}
+    layers from 2-39."""
+    shape = synth.LLAMA_13B
+    B, k = 8, 8
+    rng = np.random.default_rng(synth.BASE_SEED + 13)
+    ctx_lens = [int(x) for x in rng.integers(512, 4097, size=B)]
+    masks = [synth.random_skip_mask(shape.n_layers, 2, 39, int(rng.integers(0, 11)), stream=40 + i) for i in range(B)]
+    v = _load_verifier(shape, n_seqs=B, max_tokens=4096 + k + 8, max_nodes=k + 1, max_batch=B)
+    drafts = []
+    t0 = time.time()
+    for i in range(B):
+        toks = synth.context_tokens(shape.vocab, ctx_lens[i] + 1, stream=50 + i)
+        v.set_mask(i, masks[i])
+        v.prefill(i, toks[:-1])
+        cur = [int(toks[-1])]
+        for _ in range(k):
+            v.verify(i, cur)
+            cur.append(int(v.greedy(len(cur))[-1]))
+        drafts.append(cur)
+    log(f"13B batch: prefilled {sum(ctx_lens)} tokens and drafted in {time.time() - t0:.1f}s")
+    seqs = list(range(B))
+    inst = [[np.concatenate([[d[0]], synth.chain_draft(np.asarray(d[1:]), shape.vocab, p_accept=0.6,
+                                                        stream=1000 * j + i)]) for i, d in enumerate(drafts)]
+            for j in range(args.warmup + args.aux_steps)]
+
+    def step(j):
+        al, _ = v.verify_batch(seqs, inst[j], commit=True)
+        for i in seqs:
+            v.truncate(i, ctx_lens[i])
+        return int((al + 1).sum())
+    lat, acc = _timed(step, args.warmup, args.aux_steps)
+    out = _summary(lat, acc, batch_bytes(shape, [(masks[i], ctx_lens[i], k + 1) for i in seqs]))
+    union = np.zeros(shape.n_layers, bool)
+    for mk in masks:
+        union |= mk == 0
+    out.update({"workload": "13B-shape, batch of 8 sequences, chain k=8, contexts 512-4096, per-sequence masks",
+                "contexts": ctx_lens, "skipped_per_sequence": [int(mk.sum()) for mk in masks],
+                "blocks_launched": int(union.sum())})
+    _free(v)
+    return out
+
+
+def workload_sweep_33b(args):
+    """33B, one 4096-token context prefilled dense, 32-node tree + root (depth
+    5, branching 4,3,2,1,1, quotas 4,10,10,5,3), 64 masks of U{4..16} layers
+    from 2-59 verified back to back as dry runs (timing only)."""
+    shape = synth.LLAMA_33B
+    ctx_n = 4096
+    v = _load_verifier(shape, n_seqs=1, max_tokens=ctx_n + 40, max_nodes=33)
+    toks = synth.context_tokens(shape.vocab, ctx_n + 1, stream=5)
+    v.prefill(0, toks[:ctx_n])
+    parent = synth.topk_tree_parents((4, 3, 2, 1, 1), (4, 10, 10, 5, 3))
+
+    def greedy_of(tok, node):
+        path = [node]
+        while parent[path[-1]] >= 0:
+            path.append(int(parent[path[-1]]))
+        chain = tok[path[::-1]]
+        v.verify(0, chain)
+        return int(v.greedy(len(chain))[-1])
+    tokens = synth.tree_draft_tokens(parent, int(toks[ctx_n]), greedy_of, shape.vocab, 0.6, stream=5)
+    rng = np.random.default_rng(synth.BASE_SEED + 33)
+    masks = [synth.random_skip_mask(shape.n_layers, 2, 59, int(rng.integers(4, 17)), stream=100 + i)
+             for i in range(64)]
+    per_mask, lat_all, acc_all, by_all = [], [], [], []
+    n_steps = max(3, args.aux_steps // 10)
+    for mi, mk in enumerate(masks):
+        if mi % 16 == 0:
+            log(f"33B sweep: mask {mi}/64")
+
+        def step(i, mk=mk):
+            al, _ = v.verify(0, tokens, parent, mask=mk)
+            return al + 1
+        lat, acc = _timed(step, 1, n_steps)
+        by = batch_bytes(shape, [(mk, ctx_n, len(parent))])
+        per_mask.append((int(mk.sum()), float(np.median(lat)) * 1e6, by / PEAK_HBM / float(np.median(lat))))
+        lat_all.append(lat)
+        acc_all.append(acc)
+        by_all.append(by)
+    sk = np.array([p[0] for p in per_mask], float)
+    us = np.array([p[1] for p in per_mask])
+    slope, icpt = np.polyfit(sk, us, 1)
+    lat = np.concatenate(lat_all)
+    med = float(np.median([p[1] for p in per_mask])) * 1e-6
+    out = {"workload": "33B-shape, 32-node tree + root, 4096-token context, 64 skip masks of 4-16 layers (dry runs)",
+           "masks": 64, "steps_per_mask": n_steps, "latency_us_median": med * 1e6,
+           "latency_us_p10": float(np.percentile(us, 10)), "latency_us_p90": float(np.percentile(us, 90)),
+           "accepted_tok_s": float(np.concatenate(acc_all).sum() / lat.sum()),
+           "algorithmic_GB_mean": float(np.mean(by_all)) / 1e9,
+           "roofline_frac_median": float(np.median([p[2] for p in per_mask])),
+           "us_per_skipped_layer": float(-slope), "us_at_zero_skips_fit": float(icpt),
+           "roofline_us_per_skipped_layer": batch_bytes(shape, [(np.zeros(shape.n_layers), ctx_n, 33)]) / PEAK_HBM * 1e6
+           - batch_bytes(shape, [(synth.mask_from_layers(shape.n_layers, [2]), ctx_n, 33)]) / PEAK_HBM * 1e6,
+           "per_mask": [{"skipped": p[0], "latency_us": p[1], "roofline_frac": p[2]} for p in per_mask]}
+    _free(v)
+    return out
 
 
 def cpu_baseline(args, shape, gpu_accept_mean):
@@ -223,6 +419,9 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-reps", type=int, default=5)
+    ap.add_argument("--aux-steps", type=int, default=50, help="timed steps of the tree / batch workloads")
+    ap.add_argument("--workloads", default="tree7b,batch13b,sweep33b",
+                    help="other workloads to time after the headline one (comma list, or none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--skips", default="0,4,8", help="skip counts to time; the first is the headline")
     ap.add_argument("--calib-copy", type=float, default=0.0,
@@ -235,7 +434,7 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
               "(the verify step runs on a single MI355X)", file=sys.stderr)
         sys.exit(2)
-    shape, res, prof = run_gpu(args)
+    shape, res, prof, v7 = run_gpu(args)
     d0 = res[0]
     M = K_DRAFT + 1
     roof = None
@@ -250,6 +449,20 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args, shape, d0["mean_accept_len"])
+    workloads = {}
+    runners = {"tree7b": workload_tree_7b, "batch13b": workload_batch_13b, "sweep33b": workload_sweep_33b}
+    names = [w for w in args.workloads.split(",") if w and w != "none"]
+    for name in names:
+        if name not in runners:
+            raise SystemExit(f"unknown workload {name}; choose from {sorted(runners)}")
+    if "tree7b" not in names:
+        _free(v7)
+    for name in names:
+        log(f"workload {name}")
+        workloads[name] = workload_tree_7b(args, v7) if name == "tree7b" else runners[name](args)
+        w = workloads[name]
+        log(f"workload {name}: median {w['latency_us_median']:.0f} us, "
+            f"{w['accepted_tok_s']:.0f} accepted tok/s")
     out = {
         "metric": METRIC,
         "value": d0["accepted_tok_s"],
@@ -271,6 +484,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "by_skip": {str(k): v for k, v in res.items()},
+        "workloads": workloads,
     }
     print(json.dumps(out), flush=True)
 

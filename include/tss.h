@@ -111,7 +111,7 @@ typedef struct {
   float rope_base;     /* rotary base, 10000 for LLaMA */
   float rms_eps;       /* RMSNorm epsilon, 1e-6 */
   int32_t dtype;       /* enum tss_dtype */
-  int32_t max_nodes;   /* most nodes of one sequence in a verify (and of a prefill chunk) */
+  int32_t max_nodes;   /* most nodes of one sequence in a verify */
   int32_t max_batch;   /* most sequences of one tss_verify_batch (1 for single-sequence use) */
 } tss_model_cfg;
 
@@ -153,7 +153,8 @@ int tss_kv_alloc(tss_ctx* ctx, int32_t n_seqs, int32_t max_tokens_per_seq, void*
 int tss_set_skip_mask(tss_ctx* ctx, int32_t seq, const uint8_t* mask);
 
 /* Appends n context tokens to sequence seq under its skip mask: their K/V are
- * computed and kept for every layer the mask runs. */
+ * computed and kept for every layer the mask runs.  The tokens go through the
+ * decoder in chunks of min(64, rows of one step). */
 int tss_prefill(tss_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n);
 
 /* One verification step.

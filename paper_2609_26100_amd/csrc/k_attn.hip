@@ -242,7 +242,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     for (int w = 0; w < W; ++w) num += sm_f[w * 16 + row] * sm_o[(w * 64 + src) * OS + n * 4 + v];
     const int dim = NO * (src & 15) + n;
     if (G == 1)
-      store_act<TW>(a.o, a.o_plane, (size_t)node * a.d + head * HD + dim, num / sm_den[row]);
+      store_act<TW>(a.o, a.o_plane, act_index<TW>(node, head * HD + dim, a.d), num / sm_den[row]);
     else
       po[row * HD + dim] = num;
   }
@@ -281,7 +281,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       den += f * pm0[k * 32 + row * 2 + 1];
       num += f * po0[(size_t)k * 16 * HD + row * HD + dim];
     }
-    store_act<TW>(a.o, a.o_plane, (size_t)node * a.d + head * HD + dim, num / den);
+    store_act<TW>(a.o, a.o_plane, act_index<TW>(node, head * HD + dim, a.d), num / den);
   }
   if (threadIdx.x == 0) a.counters[tile] = 0;
 }

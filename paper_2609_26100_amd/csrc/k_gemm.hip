@@ -10,9 +10,10 @@
 //   * W is pre-packed in 1 KiB MFMA-lane-ordered tiles (tss_internal.h): every
 //     wave-wide 16-byte load reads one contiguous KiB, and a workgroup streams
 //     one strip of 16 (or 32) output columns over the full K.
-//   * The waves of a workgroup split K; each wave keeps CPW chunk loads in
-//     flight, runs the MFMAs, and the partial sums meet in LDS in a fixed
-//     order (no atomics: results are bit-reproducible).
+//   * The waves of a workgroup split K; each wave keeps a ring of chunk
+//     loads in flight (refilled as each chunk is consumed), runs the MFMAs,
+//     and the partial sums meet in LDS in a fixed order (no atomics: results
+//     are bit-reproducible).
 //   * Rows are padded to 16 for the MFMA; padded rows load nothing.
 //   * bf16: W in bf16; the fp32 activations arrive as hi and lo bf16 planes
 //     and each W tile meets both (two v_mfma_f32_16x16x32_bf16), so the
@@ -61,18 +62,23 @@ __device__ __forceinline__ uint4 load_stream(const uint8_t* p) {
   return uint4{v.x, v.y, v.z, v.w};
 }
 
-// Chunk loads in flight per wave (register budget of a 512-thread
-// workgroup: 256 VGPRs per lane, kept well below for occupancy).
-template <int MT, int NT> struct Cpw {
-  static constexpr int v = (MT == 1 && NT == 1) ? 8 : ((MT * NT) <= 2 ? 4 : ((MT * NT) <= 4 ? 2 : 1));
+// Chunks each wave keeps in flight: a ring of D slots, each holding one
+// chunk's weight tiles (NT x 4 VGPRs) and activation tiles (MT x S x 4
+// VGPRs), sized to about 160 VGPRs per lane.
+// (64 VGPRs with one row tile, where more would cost occupancy; 128 above;
+// measured on the 7B projections)
+template <int MT, int NT, int S> struct Depth {
+  static constexpr int per = NT * 4 + MT * S * 4;
+  static constexpr int raw = (MT == 1 ? 64 : 128) / per;
+  static constexpr int v = raw < 1 ? 1 : (raw > 8 ? 8 : raw);
 };
 
 template <typename T, int MT, int NT, int EPI>
 __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
   constexpr int KL = KC / 4;           // K elements per lane per tile
-  constexpr int CPW = Cpw<MT, NT>::v;
   constexpr int S = Mode<T>::planes;
+  constexpr int D = Depth<MT, NT, S>::v;
   using KV = typename Mode<T>::KV;
   constexpr int ROWS = MT * 16;
   constexpr int COLS = NT * 16;
@@ -120,33 +126,73 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     ssv[i] = (ss_early && wave < M && p < a.ss_nparts) ? a.ss_in[(size_t)wave * a.ss_stride + p] : 0.f;
   }
 
-  for (int base = wave * CPW; base < nkc; base += waves * CPW) {
-    uint4 wv[CPW][NT];
-    uint4 xv[CPW][MT][S];
+  // Wave w takes chunks w, w + waves, w + 2 waves, ... (adjacent waves read
+  // adjacent KiB).  Software pipeline: a ring of D slots, each refilled with
+  // the chunk D steps ahead as soon as it is consumed, so D chunks stay in
+  // flight through the K loop.  Activation loads are issued with their
+  // chunk's weight loads (loads complete in order, so waiting on one slot
+  // never waits on a later chunk).  The loads carry no conditions (the
+  // counter-based waits stay exact): padded rows re-read row M-1 (their
+  // products land in output rows that are never stored) and the main loop
+  // only runs while every refill is in range; the last chunks are finished
+  // by a short tail.
+  const int n_my = wave < nkc ? (nkc - wave + waves - 1) / waves : 0;
+  uint4 wv[D][NT];
+  uint4 xv[D][MT][S];
+  // Activation tiles through a buffer resource: a padded row (>= M) gets an
+  // offset past the buffer's end, which the hardware answers with zeros
+  // without touching memory (no branch, so the load-count waits stay exact).
+  const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)x, (short)0, (int)((size_t)S * (a.x_plane > 0 ? a.x_plane : (size_t)a.Mp * K) * sizeof(T)), 0x00020000);
+  constexpr int kPastEnd = 1 << 30;
+  int xoff[MT];
 #pragma unroll
-    for (int i = 0; i < CPW; ++i) {
-      const int c = base + i;
-      const bool in = c < nkc;
+  for (int mt = 0; mt < MT; ++mt)
+    xoff[mt] = mt * 16 + r16 < M ? (mt * nkc * 64 + lane) * 16 : kPastEnd;
+  const int plane_bytes = (int)(a.x_plane * sizeof(T));
+  auto issue = [&](uint4 (&w)[NT], uint4 (&xs)[MT][S], int i) {
+    const int c = wave + i * waves;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) w[nt] = load_stream(wstrip + ((size_t)c * NT + nt) * kTileBytes);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int p = 0; p < S; ++p) {
+        typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+        const u4v v = __builtin_amdgcn_raw_buffer_load_b128(xres, xoff[mt] + c * kTileBytes + p * plane_bytes, 0, 0);
+        xs[mt][p] = uint4{v.x, v.y, v.z, v.w};
+      }
+  };
+  auto compute = [&](uint4 (&w)[NT], uint4 (&xs)[MT][S]) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        wv[i][nt] = in ? load_stream(wstrip + ((size_t)c * NT + nt) * kTileBytes) : uint4{0, 0, 0, 0};
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + r16;
-        const size_t off = (size_t)m * K + (size_t)c * KC + grp * KL;
+        for (int p = 0; p < S; ++p) acc[mt][nt] = mfma_chunk<T>(xs[mt][p], w[nt], acc[mt][nt]);
+  };
+  if (n_my > 0) {
 #pragma unroll
-        for (int p = 0; p < S; ++p)
-          xv[i][mt][p] = (in && m < M) ? *(const uint4*)(x + p * a.x_plane + off) : uint4{0, 0, 0, 0};
+    for (int j = 0; j < D; ++j) issue(wv[j], xv[j], min(j, n_my - 1));
+    int i0 = 0;
+    for (; i0 + 2 * D <= n_my; i0 += D) {
+#pragma unroll
+      for (int j = 0; j < D; ++j) {
+        compute(wv[j], xv[j]);
+        issue(wv[j], xv[j], i0 + j + D);
+      }
+    }
+    // tail: fewer than 2 D chunks left, the first D of them already in the ring
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      if (i0 + j < n_my) {
+        compute(wv[j], xv[j]);
+        if (i0 + j + D < n_my) issue(wv[j], xv[j], i0 + j + D);
       }
     }
 #pragma unroll
-    for (int i = 0; i < CPW; ++i)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int p = 0; p < S; ++p) acc[mt][nt] = mfma_chunk<T>(xv[i][mt][p], wv[i][nt], acc[mt][nt]);
+    for (int j = 0; j < D; ++j)
+      if (i0 + D + j < n_my) compute(wv[j], xv[j]);
   }
 
   // LDS: red[waves][ROWS][COLS] | y[ROWS][COLS] | rscale[ROWS] | aux[ROWS][COLS]
@@ -243,7 +289,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       const size_t idx = (size_t)row * N + n0 + col;
       const float hn = a.h[idx] + yfin[row * COLS + col];
       a.h[idx] = hn;
-      store_act<T>(a.xn, a.xn_plane, idx, hn * a.g_next[s_seq[row]][n0 + col]);
+      store_act<T>(a.xn, a.xn_plane, act_index<T>(row, n0 + col, N), hn * a.g_next[s_seq[row]][n0 + col]);
       aux[row * COLS + col] = hn * hn;
     }
     __syncthreads();
@@ -260,7 +306,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       const int row = e >> 4, c = e & 15;
       const float g = yfin[row * COLS + c];
       const float u = yfin[row * COLS + 16 + c];
-      store_act<T>(a.act, a.act_plane, (size_t)row * F + strip * 16 + c, silu(g) * u);
+      store_act<T>(a.act, a.act_plane, act_index<T>(row, strip * 16 + c, F), silu(g) * u);
     }
   } else {  // EPI_LOGITS
     const int N = a.N;
@@ -319,13 +365,10 @@ template <typename T, int MT>
 static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
   const int nt = strip_tiles(epi);
   const int strips = a.N / (16 * nt);
-  const int cpw = nt == 2 ? Cpw<MT, 2>::v : Cpw<MT, 1>::v;
-  // enough waves to cover K with CPW-chunk blocks, capped by LDS and 8
-  // (8-wave workgroups measured best across the 7B shapes); up to 64 rows the
-  // reduction stays within 64 KiB
+  // 8 waves (measured best across the 7B shapes) unless K is short, capped by
+  // LDS: up to 64 rows the cross-wave reduction stays within 64 KiB
   const size_t cap = MT <= 4 ? 65536 : kGemmLdsMax;
-  int waves = (a.nkc + cpw - 1) / cpw;
-  if (waves > 8) waves = 8;
+  int waves = a.nkc < 8 ? a.nkc : 8;
   auto lds_of = [&](int w) { return nt == 2 ? gemm_lds<MT, 2>(w) : gemm_lds<MT, 1>(w); };
   while (waves > 1 && lds_of(waves) > cap) waves >>= 1;
   const size_t lds = lds_of(waves);

@@ -43,7 +43,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
       const int k = c * E + j;
       const float v = (float)e[j];
       a.h[(size_t)m * d + k] = v;
-      store_act<T>(a.xn, a.xn_plane, (size_t)m * d + k, v * gain[k]);
+      store_act<T>(a.xn, a.xn_plane, act_index<T>(m, k, d), v * gain[k]);
       rowv[k] = v;
     }
   }

@@ -1129,7 +1129,8 @@ int tss_prefill(tss_ctx* c, int32_t seq, const int32_t* tokens, int32_t n) {
   for (int l = 0; l < L; ++l)
     if (!c->mask[seq][l] && c->kv_len[seq][l] != c->n_kv[seq])
       return fail(c, TSS_ESTATE, "an active layer lacks K/V for the committed context");
-  const int chunk = std::min({c->cfg.max_nodes, kMaxNodes, row_cap(&c->cfg)});
+  // chunks as large as the step's rows allow (a chain of at most 64 nodes)
+  const int chunk = std::min(kMaxNodes, row_cap(&c->cfg));
   tss_ctx::Step& st = c->step;
   st.n_seqs = 1;
   st.seq[0] = seq;

@@ -2,6 +2,10 @@
 //
 // Device data layout (all buffers owned by the caller):
 //
+//   projection inputs (the activation planes of h * gain, attention output,
+//   SwiGLU output) are stored tile by tile in MFMA A-operand order
+//   (act_index below), Mp rows (a multiple of 16) x K columns per plane.
+//
 //   packed weights  embed [V][d] (T, row-major, gathered by token id);
 //                   per layer: attn_norm [d] f32, W_qkv packed, W_o packed,
 //                   mlp_norm [d] f32, W_gateup packed, W_down packed;
@@ -59,6 +63,18 @@ template <> struct Mode<float> {
   static constexpr int planes = 1;
 };
 
+// Index of element (row, k) of a projection input with K columns (K a
+// multiple of the tile width KC = 64 / sizeof(T)), in MFMA A-operand tile
+// order: the 16 x KC tile (row / 16, k / KC) is one contiguous KiB whose lane
+// l = (k % KC) / (KC / 4) * 16 + row % 16 holds KC / 4 consecutive k, so a
+// wave reads a whole tile with one 16-byte load per lane.
+template <typename T>
+__device__ __forceinline__ size_t act_index(int row, int k, int K) {
+  constexpr int KC = 64 / (int)sizeof(T), KL = KC / 4;
+  const int nkc = K / KC;
+  return (((size_t)(row >> 4) * nkc + k / KC) * 64 + (k % KC) / KL * 16 + (row & 15)) * KL + (k % KL);
+}
+
 // Stores an fp32 activation in the mode's plane format.
 template <typename T>
 __device__ __forceinline__ void store_act(void* base, size_t plane, size_t idx, float v) {
@@ -103,7 +119,7 @@ enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 
 struct GemmArgs {
   const uint8_t* w;        // packed weights of this matrix
-  const void* x;           // A operand rows [M][K] of T (row stride K), planes x_plane apart
+  const void* x;           // A operand [Mp][K] of T in tile order (act_index), planes x_plane elements apart
   size_t x_plane;
   int M, K, N;             // N = packed output columns
   int nkc;                 // K / KC
