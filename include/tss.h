@@ -70,9 +70,9 @@ enum tss_flags {
 enum tss_launch_mode {
   TSS_LAUNCH_DIRECT = 0, /* one launch per kernel */
   TSS_LAUNCH_GRAPH = 1   /* default: the step's launches are captured once per step shape
-                            (sequence, skip mask, node count, tree or chain, attention
-                            workgroups) into a HIP graph and replayed; results are
-                            bit-identical to direct launches */
+                            (sequences, skip masks, node counts, tree-path compaction;
+                            not context lengths) into a HIP graph and replayed; results
+                            are bit-identical to direct launches */
 };
 
 /* Kernel kinds for tss_profile_kernel. */

@@ -58,8 +58,18 @@ int round16(int x) { return (x + 15) & ~15; }
 int row_cap(const tss_model_cfg* c) {
   return std::min(c->max_nodes * c->max_batch, c->dtype == TSS_BF16 ? kMaxRows : 64);
 }
-// 16-row attention tiles one step can carry (tiles never straddle sequences)
-int tile_cap(const tss_model_cfg* c) { return std::min(kMaxTiles, (row_cap(c) + 15 * c->max_batch) / 16); }
+// Attention workgroups per (head, sequence) when n_seq sequences run a block:
+// at most about kAttnTargetWGs workgroups in all (at least one per pair).
+int attn_groups(int n_heads, int n_seq) {
+  return std::max(1, std::min(kAttnMaxGroups, kAttnTargetWGs / (n_heads * n_seq)));
+}
+// partial-state slots of one attention launch: n_heads * n_seq * groups over
+// every n_seq (at most max(kAttnTargetWGs, n_heads * n_seq))
+size_t attn_slots(const tss_model_cfg* c) {
+  size_t m = 0;
+  for (int n = 1; n <= c->max_batch; ++n) m = std::max(m, (size_t)c->n_heads * n * attn_groups(c->n_heads, n));
+  return m;
+}
 
 int cfg_ok(const tss_model_cfg* c) {
   if (!c) return 0;
@@ -114,10 +124,10 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   w.q = take(Mp * d * 4);
   w.o = take(ap * Mp * d * es);
   w.act = take(ap * Mp * f * es);
-  const size_t tiles = (size_t)c->n_heads * tile_cap(c);
-  w.part_o = take(tiles * kAttnMaxGroups * 16 * c->head_dim * 4);
-  w.part_ml = take(tiles * kAttnMaxGroups * 16 * 2 * 4);
-  w.counters = take(tiles * 4);
+  const size_t slots = attn_slots(c);
+  w.part_o = take(slots * kAttnMaxTiles * 16 * c->head_dim * 4);
+  w.part_ml = take(slots * kAttnMaxTiles * 16 * 2 * 4);
+  w.counters = take((size_t)c->n_heads * kMaxBatch * 4);
   w.logits = take(Mp * v * 4);
   w.am_val = take((v / 16) * Mp * 4);
   w.am_idx = take((v / 16) * Mp * 4);
@@ -376,7 +386,7 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
   if (e == hipSuccess) step("mapped result address", hipHostGetDevicePointer((void**)&c->res_dev_map, c->res_host, 0));
   if (e == hipSuccess)
     step("attention counters",
-         hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * tile_cap(cfg) * 4, c->stream));
+         hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * kMaxBatch * 4, c->stream));
   if (e == hipSuccess) step("stream sync", hipStreamSynchronize(c->stream));
   if (e == hipSuccess) step("attention LDS attribute", init_kernel_attributes());
   if (e == hipSuccess) step("projection LDS attribute", init_gemm_attributes());
@@ -634,21 +644,6 @@ struct ProfScope {
 
 EmbedArgs embed_args(tss_ctx* c);
 
-int attn_groups_for(int n_kv, int M) {
-  const int n_pages = (n_kv + M + kPage - 1) / kPage;
-  return std::max(1, std::min(kAttnMaxGroups, (n_pages + 15) / 16));
-}
-
-// Attention workgroups per (head, tile) of the step: sized for its longest
-// sequence (context + nodes).
-int step_attn_groups(const tss_ctx* c) {
-  const StepParams& sp = *c->sp_host;
-  int g = 1;
-  for (int i = 0; i < sp.n_seqs; ++i)
-    g = std::max(g, attn_groups_for(sp.seq_nkv[i], sp.seq_row0[i + 1] - sp.seq_row0[i]));
-  return g;
-}
-
 // Layer after `l` that sequence i runs (n_layers = none), and the gain of the
 // RMSNorm that layer (or the final norm) applies first.
 int next_active(const tss_ctx* c, int i, int l) {
@@ -666,11 +661,11 @@ const float* attn_gain_of(const tss_ctx* c, int layer) {
 // verify) lm_head + accept (+ KV compaction) for the rows in c->sp_host and
 // the sequences in c->step, on stream s.  A block that every sequence skips
 // is not launched; inside a launched block the rows of sequences that skip it
-// are left untouched (their attention tiles are not even listed).  Every
+// are left untouched (attention does not even list those sequences).  Every
 // kernel argument except the embedding kernel's step parameters depends only
-// on the step's shape (sequences, masks, node counts, compaction, attention
-// groups), so a captured sequence of launches can be replayed for later steps
-// of the same shape.
+// on the step's shape (sequences, masks, node counts, compaction), not on
+// context lengths, so a captured sequence of launches can be replayed for
+// later steps of the same shape.
 int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
   const tss_model_cfg& cf = c->cfg;
   const StepParams& sp = *c->sp_host;
@@ -715,25 +710,19 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
   base.sp = sp_dev;
   base.row_on[0] = base.row_on[1] = ~0ull;
 
-  const int attn_groups = step_attn_groups(c);
-
   for (int l = 0; l < L; ++l) {
-    // rows and attention tiles of the sequences that run block l
+    // rows and sequences that run block l
     uint64_t row_on[kMaxRows / 64] = {0, 0};
     AttnArgs at{};
-    int n_tiles = 0;
+    int n_act = 0, max_tiles = 1;
     for (int i = 0; i < B; ++i) {
       if (st.mask[(size_t)i * L + l]) continue;
       const int r0 = sp.seq_row0[i], r1 = sp.seq_row0[i + 1];
       for (int r = r0; r < r1; ++r) row_on[r >> 6] |= 1ull << (r & 63);
-      for (int t0 = r0; t0 < r1; t0 += 16) {
-        at.tile_row0[n_tiles] = (int16_t)t0;
-        at.tile_rows[n_tiles] = (uint8_t)std::min(16, r1 - t0);
-        at.tile_seq[n_tiles] = (uint8_t)i;
-        ++n_tiles;
-      }
+      at.seq_list[n_act++] = (uint8_t)i;
+      max_tiles = std::max(max_tiles, (r1 - r0 + 15) / 16);
     }
-    if (n_tiles == 0) continue;  // every sequence skips this block
+    if (n_act == 0) continue;  // every sequence skips this block
     const LayerW& W = c->wl.layers[l];
     GemmArgs lb = base;
     lb.row_on[0] = row_on[0];
@@ -777,14 +766,14 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
       a.part_o = (float*)(ws + c->wsl.part_o);
       a.part_ml = (float*)(ws + c->wsl.part_ml);
       a.counters = (int*)(ws + c->wsl.counters);
-      a.groups = attn_groups;
+      a.groups = attn_groups(H, n_act);
       a.layer = l;
       a.n_pages_pool = c->kvl.n_pages;
       a.n_heads = H;
       a.d = d;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
       ProfScope ps(c, TSS_K_ATTN, l);
-      HIPCHK(launch_attn(c->bf16, hd, n_tiles, a, s), "attention");
+      HIPCHK(launch_attn(c->bf16, hd, max_tiles, n_act, a, s), "attention");
       ps.done();
     }
     {  // O projection + residual; next norm input (this block's MLP norm)
@@ -950,7 +939,6 @@ int run_verify_graph(tss_ctx* c) {
     put(sp.seq_row0[i + 1] - sp.seq_row0[i]);
     put(st.compact[i]);
   }
-  put(step_attn_groups(c));
   key.append((const char*)st.mask.data(), st.mask.size());
   tss_ctx::GraphEntry* g = nullptr;
   for (auto& e : c->graphs)

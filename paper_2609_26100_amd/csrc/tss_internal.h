@@ -47,10 +47,16 @@ constexpr int kPage = 16;          // tokens per KV page
 constexpr int kMaxNodes = 64;      // nodes of one sequence in one step (u64 ancestor masks)
 constexpr int kMaxBatch = 8;       // sequences of one step
 constexpr int kMaxRows = 128;      // rows (nodes of every sequence) of one step
-constexpr int kMaxTiles = 16;      // 16-row attention tiles of one step (per-sequence tiles)
 constexpr int kMaxLayers = 256;
 constexpr int kTileBytes = 1024;   // one packed 16 x KC weight tile
-constexpr int kAttnMaxGroups = 16; // workgroups per (head, node tile) in attention
+constexpr int kAttnMaxGroups = 16; // workgroups per (head, sequence) in attention
+constexpr int kAttnMaxTiles = 4;   // 16-node tiles of one sequence in attention (kMaxNodes / 16)
+// attention workgroups one launch aims for: one round, a little under one
+// per CU (measured best on the 7B, 13B and 33B shapes)
+#ifndef TSS_ATTN_TARGET_WGS
+#define TSS_ATTN_TARGET_WGS 208
+#endif
+constexpr int kAttnTargetWGs = TSS_ATTN_TARGET_WGS;
 constexpr int kArgPages = 256;     // page ids passed in kernel arguments (one sequence, up to 4096 tokens)
 
 template <typename T> struct Mode;
@@ -162,23 +168,20 @@ struct GemmArgs {
 };
 
 struct AttnArgs {
-  const float* q;          // [Mp][d]
+  const float* q;          // [Mp][d] row-major
   const uint8_t* kv_pages;
   const int32_t* page_table;
   const StepParams* sp;
-  void* o;                 // [Mp][d] activation planes of the attention output
+  void* o;                 // activation planes of the attention output (act_index order)
   size_t o_plane;
-  float* part_o;           // [H * kMaxTiles][groups][16][hd] unnormalised partial outputs
-  float* part_ml;          // [H * kMaxTiles][groups][16][2] (max in log2 units, sum)
-  int* counters;           // [H * kMaxTiles] arrivals, zero between launches
-  int groups;              // workgroups per (head, node tile)
+  // partial states, slot ((head * n_seq + y) * groups + g), kAttnMaxTiles tiles each
+  float* part_o;           // [slots][kAttnMaxTiles][16][hd] unnormalised partial outputs
+  float* part_ml;          // [slots][kAttnMaxTiles][16][2] (max in log2 units, sum)
+  int* counters;           // [H * kMaxBatch] arrivals, zero between launches
+  int groups;              // most workgroups per (head, sequence)
   int layer, n_pages_pool, n_heads, d;
   float scale_log2;        // log2(e) / sqrt(hd)
-  // node tiles of the sequences that run this block: tile t covers rows
-  // tile_row0[t] .. + tile_rows[t] - 1, all of sequence tile_seq[t]
-  int16_t tile_row0[kMaxTiles];
-  uint8_t tile_rows[kMaxTiles];
-  uint8_t tile_seq[kMaxTiles];
+  uint8_t seq_list[kMaxBatch];  // grid.y -> sequence (those that run this block)
   int32_t pt_off[kMaxBatch];
   int32_t n_arg_pages;     // with one sequence: valid entries of pages[]
   int32_t pages[kArgPages];  // physical ids of the first pages of a single sequence
@@ -242,7 +245,7 @@ LaunchTiming& launch_timing();
 
 // Launchers (defined in the .hip files).  T is selected by `bf16`.
 hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_t s);
-hipError_t launch_attn(bool bf16, int head_dim, int qt, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn(bool bf16, int head_dim, int max_tiles, int n_seq, const AttnArgs& a, hipStream_t s);
 hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_compact(bool bf16, int n_seqs, const CompactArgs& a, hipStream_t s);
