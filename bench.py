@@ -64,6 +64,32 @@ def batch_bytes(shape, seqs):
     return int(union.sum()) * (2 * (4 * d * d + 3 * d * f) + 4 * d) + kv + 2 * v * d + 2 * M * d + 2 * d + 4 * M * v
 
 
+# HBM traffic of one gate/up launch (7B shape, 6 rows), from two rocprofv3
+# --pmc passes (FETCH_SIZE, then WRITE_SIZE) over
+#   bench.py --steps 5 --warmup 1 --no-cpu-baseline --skips 0 --workloads none --calib-copy 1
+# KiB per dispatch, mean of the last 64 gate/up dispatches.  The same counters
+# read 524320.9 KiB (FETCH) and 1048576.0 KiB (WRITE) for the 1 GiB device copy
+# that run makes, so FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  The
+# figures hold for the kernel sources hashed here; any change to them voids
+# the traffic field until the counters are taken again.
+GATEUP_COUNTERS = {"fetch_kib": 88650.0, "write_kib": 258.0, "fetch_scale": 2.0, "write_scale": 1.0,
+                   "sources": ("paper_2609_26100_amd/csrc/k_gemm.hip", "paper_2609_26100_amd/csrc/tss_internal.h"),
+                   "sha256": "bca71d6a0ce7439ad96956beed064983efed9c2d98f2ed7db6df4ad499955c66"}
+
+
+def gateup_traffic():
+    """Measured HBM bytes per gate/up launch, or None if the kernel changed since."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in GATEUP_COUNTERS["sources"]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != GATEUP_COUNTERS["sha256"]:
+        return None
+    c = GATEUP_COUNTERS
+    return (c["fetch_kib"] * c["fetch_scale"] + c["write_kib"] * c["write_scale"]) * 1024
+
+
 def gateup_bytes(shape, M):
     """Algorithmic bytes of one gate/up launch: W_gate and W_up (bf16), the
     normalised input rows, the SwiGLU output rows."""
@@ -444,7 +470,7 @@ def main():
         achieved = gb / avg_s / 1e9
         roof = {"kernel": "gate/up projection + SwiGLU (layer 0, dense)", "bound": "hbm",
                 "achieved": achieved, "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": achieved / (PEAK_HBM / 1e9),
-                "traffic": None, "avg_launch_us": avg_s * 1e6, "launches": prof[1],
+                "traffic": gateup_traffic(), "avg_launch_us": avg_s * 1e6, "launches": prof[1],
                 "algorithmic_bytes_per_launch": gb}
     cpu = None
     if not args.no_cpu_baseline:
