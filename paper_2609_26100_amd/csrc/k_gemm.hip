@@ -89,7 +89,21 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   const int r16 = lane & 15, grp = lane >> 4;
   const int strip = blockIdx.x;
   const int M = a.M, K = a.K, nkc = a.nkc;
-  const uint8_t* wstrip = a.w + (size_t)strip * nkc * NT * kTileBytes + lane * 16;
+  // weight tile nt of this strip, chunk c, at wb[nt] + c * wstep: plain
+  // matrices store a 16-row tile's chunks consecutively; gate and up tiles of
+  // one pair alternate chunk by chunk
+  const uint8_t* wb[NT];
+  size_t wstep;
+  if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      wb[nt] = a.w + (((size_t)(strip * (NT / 2) + nt / 2) * nkc * 2) + (nt & 1)) * kTileBytes + lane * 16;
+    wstep = 2 * kTileBytes;
+  } else {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) wb[nt] = a.w + (size_t)(strip * NT + nt) * nkc * kTileBytes + lane * 16;
+    wstep = kTileBytes;
+  }
   const T* x = (const T*)a.x;
 
   f32x4 acc[MT][NT];
@@ -153,7 +167,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   auto issue = [&](uint4 (&w)[NT], uint4 (&xs)[MT][S], int i) {
     const int c = wave + i * waves;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) w[nt] = load_stream(wstrip + ((size_t)c * NT + nt) * kTileBytes);
+    for (int nt = 0; nt < NT; ++nt) w[nt] = load_stream(wb[nt] + (size_t)c * wstep);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -195,11 +209,13 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       if (i0 + D + j < n_my) compute(wv[j], xv[j]);
   }
 
-  // LDS: red[waves][ROWS][COLS] | y[ROWS][COLS] | rscale[ROWS] | aux[ROWS][COLS]
+  // LDS: red[max(waves, 2)][ROWS][COLS] | rscale[ROWS].  The sum over waves
+  // lands in red's first slice (yfin: each element is read and written by
+  // one thread) and the residual epilogue's squares in its second (aux).
   float* red = smem;
-  float* yfin = red + waves * ROWS * COLS;
-  float* rscale = yfin + ROWS * COLS;
-  float* aux = rscale + ROWS;
+  float* yfin = red;
+  float* aux = red + ROWS * COLS;
+  float* rscale = red + (waves < 2 ? 2 : waves) * ROWS * COLS;
 
   // MFMA result layout: lane holds column r16, rows 4*grp + v.
 #pragma unroll
@@ -211,30 +227,15 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
         red[(wave * ROWS + mt * 16 + grp * 4 + v) * COLS + nt * 16 + r16] = acc[mt][nt][v];
 
   // RMSNorm row scale from the producer's partial sums (fixed order, so every
-  // workgroup derives the same value).
-  if (ss_early) {
-    if (wave < M) {
-      float s = 0.f;
+  // workgroup derives the same value): here when each row has its own wave
+  // (loaded before the weight stream), otherwise below.
+  if (ss_early && wave < M) {
+    float s = 0.f;
 #pragma unroll
-      for (int i = 0; i < SSV; ++i) s += ssv[i];
+    for (int i = 0; i < SSV; ++i) s += ssv[i];
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-      if (lane == 0) rscale[wave] = rsqrtf(s / (float)a.norm_dim + a.eps);
-    }
-  } else if (a.ss_in) {
-    for (int m = wave; m < M; m += waves) {
-      float s = 0.f;
-#pragma unroll
-      for (int i = 0; i < SSV; ++i) {
-        const int p = lane + 64 * i;
-        s += p < a.ss_nparts ? a.ss_in[(size_t)m * a.ss_stride + p] : 0.f;
-      }
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-      if (lane == 0) rscale[m] = rsqrtf(s / (float)a.norm_dim + a.eps);
-    }
-  } else {
-    for (int m = threadIdx.x; m < M; m += blockDim.x) rscale[m] = 1.f;
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+    if (lane == 0) rscale[wave] = rsqrtf(s / (float)a.norm_dim + a.eps);
   }
   __syncthreads();
 
@@ -242,8 +243,41 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     const int row = e / COLS, col = e % COLS;
     float s = 0.f;
     for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * COLS + col];
-    yfin[row * COLS + col] = s * rscale[row];
+    yfin[row * COLS + col] = s;
   }
+
+  if (!ss_early) {
+    if (a.ss_in) {
+      // rows in groups of 4 per wave, every load of a group issued together
+      // (indices clamped, out-of-range parts weighted 0)
+      for (int m0 = wave; m0 < M; m0 += 4 * waves) {
+        float sum[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = min(m0 + r * waves, M - 1);
+          float v[SSV];
+#pragma unroll
+          for (int i = 0; i < SSV; ++i) v[i] = a.ss_in[(size_t)m * a.ss_stride + min(lane + 64 * i, a.ss_nparts - 1)];
+          float t = 0.f;
+#pragma unroll
+          for (int i = 0; i < SSV; ++i) t += lane + 64 * i < a.ss_nparts ? v[i] : 0.f;
+          sum[r] = t;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float t = sum[r];
+#pragma unroll
+          for (int off = 32; off >= 1; off >>= 1) t += __shfl_xor(t, off);
+          const int m = m0 + r * waves;
+          if (lane == 0 && m < M) rscale[m] = rsqrtf(t / (float)a.norm_dim + a.eps);
+        }
+      }
+    } else {
+      for (int m = threadIdx.x; m < M; m += blockDim.x) rscale[m] = 1.f;
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) yfin[e] *= rscale[e / COLS];
   __syncthreads();
 
   const int n0 = strip * COLS;
@@ -293,20 +327,23 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       aux[row * COLS + col] = hn * hn;
     }
     __syncthreads();
-    for (int row = threadIdx.x; row < M; row += blockDim.x) {
+    // one partial sum of h^2 per 16 columns (the format every norm reads)
+    for (int e = threadIdx.x; e < M * NT; e += blockDim.x) {
+      const int row = e / NT, j = e % NT;
       if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
       float s = 0.f;
-      for (int col = 0; col < COLS; ++col) s += aux[row * COLS + col];
-      a.ss_out[(size_t)row * a.ss_stride + strip] = s;
+      for (int col = j * 16; col < j * 16 + 16; ++col) s += aux[row * COLS + col];
+      a.ss_out[(size_t)row * a.ss_stride + strip * NT + j] = s;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
-    static_assert(NT == 2, "gate and up tiles pair up in one strip");
+    static_assert(NT % 2 == 0, "gate and up tiles pair up");
     const int F = a.N >> 1;
-    for (int e = threadIdx.x; e < M * 16; e += blockDim.x) {
-      const int row = e >> 4, c = e & 15;
-      const float g = yfin[row * COLS + c];
-      const float u = yfin[row * COLS + 16 + c];
-      store_act<T>(a.act, a.act_plane, act_index<T>(row, strip * 16 + c, F), silu(g) * u);
+    constexpr int PAIRS = NT / 2;
+    for (int e = threadIdx.x; e < M * 16 * PAIRS; e += blockDim.x) {
+      const int row = e / (16 * PAIRS), j = (e / 16) % PAIRS, c = e & 15;
+      const float g = yfin[row * COLS + j * 32 + c];
+      const float u = yfin[row * COLS + j * 32 + 16 + c];
+      store_act<T>(a.act, a.act_plane, act_index<T>(row, (strip * PAIRS + j) * 16 + c, F), silu(g) * u);
     }
   } else {  // EPI_LOGITS
     const int N = a.N;
@@ -314,15 +351,17 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       const int row = e / COLS, col = e % COLS;
       a.logits[(size_t)row * N + n0 + col] = yfin[row * COLS + col];
     }
-    for (int row = threadIdx.x; row < M; row += blockDim.x) {
-      float bv = yfin[row * COLS];
-      int bi = 0;
-      for (int col = 1; col < COLS; ++col) {
+    // one (max, argmax) per 16 columns, lowest column on ties
+    for (int e = threadIdx.x; e < M * NT; e += blockDim.x) {
+      const int row = e / NT, j = e % NT;
+      float bv = yfin[row * COLS + j * 16];
+      int bi = j * 16;
+      for (int col = j * 16 + 1; col < j * 16 + 16; ++col) {
         const float v = yfin[row * COLS + col];
         if (v > bv) { bv = v; bi = col; }
       }
-      a.am_val[(size_t)row * a.am_stride + strip] = bv;
-      a.am_idx[(size_t)row * a.am_stride + strip] = n0 + bi;
+      a.am_val[(size_t)row * a.am_stride + strip * NT + j] = bv;
+      a.am_idx[(size_t)row * a.am_stride + strip * NT + j] = n0 + bi;
     }
   }
 }
@@ -333,7 +372,7 @@ constexpr size_t kGemmLdsMax = 152 * 1024;
 
 template <int MT, int NT>
 constexpr size_t gemm_lds(int waves) {
-  return (size_t)(waves * MT * 16 * NT * 16 + MT * 16 * NT * 16 * 2 + MT * 16) * 4;
+  return (size_t)((waves < 2 ? 2 : waves) * MT * 16 * NT * 16 + MT * 16) * 4;
 }
 
 template <typename T, int MT, int NT, int EPI>
@@ -342,67 +381,97 @@ static hipError_t gemm_attr() {
                              (int)kGemmLdsMax);
 }
 
-template <typename T, int MT>
+template <typename T, int MT, int NT>
 static hipError_t gemm_attr_mt() {
-  hipError_t e = gemm_attr<T, MT, 1, EPI_QKV>();
-  if (e == hipSuccess) e = gemm_attr<T, MT, 1, EPI_RESID>();
-  if (e == hipSuccess) e = gemm_attr<T, MT, 2, EPI_SWIGLU>();
-  if (e == hipSuccess) e = gemm_attr<T, MT, 1, EPI_LOGITS>();
+  hipError_t e = gemm_attr<T, MT, NT, EPI_QKV>();
+  if (e == hipSuccess) e = gemm_attr<T, MT, NT, EPI_RESID>();
+  if (e == hipSuccess) e = gemm_attr<T, MT, NT < 2 ? 2 : NT, EPI_SWIGLU>();
+  if (e == hipSuccess) e = gemm_attr<T, MT, NT, EPI_LOGITS>();
   return e;
 }
 
 // Lets the many-row variants use more than 64 KiB of LDS for the cross-wave
 // reduction (called once at context creation).
-hipError_t init_gemm_attributes() {
-  hipError_t e = gemm_attr_mt<__bf16, 5>();
-  if (e == hipSuccess) e = gemm_attr_mt<__bf16, 6>();
-  if (e == hipSuccess) e = gemm_attr_mt<__bf16, 7>();
-  if (e == hipSuccess) e = gemm_attr_mt<__bf16, 8>();
+template <typename T, int MT>
+static hipError_t gemm_attr_rows() {
+  hipError_t e = gemm_attr_mt<T, MT, 1>();
+  if (e == hipSuccess) e = gemm_attr_mt<T, MT, 2>();
+  if (e == hipSuccess) e = gemm_attr_mt<T, MT, 4>();
   return e;
 }
 
-template <typename T, int MT>
-static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
-  const int nt = strip_tiles(epi);
-  const int strips = a.N / (16 * nt);
+hipError_t init_gemm_attributes() {
+  hipError_t e = gemm_attr_rows<__bf16, 1>();
+  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 2>();
+  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 3>();
+  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 4>();
+  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 5>();
+  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 6>();
+  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 7>();
+  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 8>();
+  if (e == hipSuccess) e = gemm_attr_rows<float, 1>();
+  if (e == hipSuccess) e = gemm_attr_rows<float, 2>();
+  if (e == hipSuccess) e = gemm_attr_rows<float, 3>();
+  if (e == hipSuccess) e = gemm_attr_rows<float, 4>();
+  return e;
+}
+
+template <typename T, int MT, int NT, int EPI>
+static hipError_t launch_v(const GemmArgs& a, hipStream_t s) {
   // 8 waves (measured best across the 7B shapes) unless K is short, capped by
   // LDS: up to 64 rows the cross-wave reduction stays within 64 KiB
-  const size_t cap = MT <= 4 ? 65536 : kGemmLdsMax;
+  // (4-tile blocks and more than 4 row tiles may use most of the CU's LDS)
+  const size_t cap = (MT == 1 || (MT <= 4 && NT <= 2)) ? 65536 : kGemmLdsMax;
   int waves = a.nkc < 8 ? a.nkc : 8;
-  auto lds_of = [&](int w) { return nt == 2 ? gemm_lds<MT, 2>(w) : gemm_lds<MT, 1>(w); };
-  while (waves > 1 && lds_of(waves) > cap) waves >>= 1;
-  const size_t lds = lds_of(waves);
-  dim3 grid(strips), block(waves * 64);
-  switch (epi) {
-    case EPI_QKV: TSS_LAUNCH((k_gemm<T, MT, 1, EPI_QKV>), grid, block, lds, s, a); break;
-    case EPI_RESID: TSS_LAUNCH((k_gemm<T, MT, 1, EPI_RESID>), grid, block, lds, s, a); break;
-    case EPI_SWIGLU: TSS_LAUNCH((k_gemm<T, MT, 2, EPI_SWIGLU>), grid, block, lds, s, a); break;
-    default: TSS_LAUNCH((k_gemm<T, MT, 1, EPI_LOGITS>), grid, block, lds, s, a); break;
-  }
+  while (waves > 1 && gemm_lds<MT, NT>(waves) > cap) waves >>= 1;
+  const size_t lds = gemm_lds<MT, NT>(waves);
+  dim3 grid(a.N / (16 * NT)), block(waves * 64);
+  TSS_LAUNCH((k_gemm<T, MT, NT, EPI>), grid, block, lds, s, a);
   return hipGetLastError();
 }
 
-// mt = 16-row tiles of the step's rows: up to 8 (128 rows) in the bf16 mode,
-// up to 4 (64 rows) in the f32 mode.
-hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_t s) {
+template <typename T, int MT, int NT>
+static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
+  switch (epi) {
+    case EPI_QKV: return launch_v<T, MT, NT, EPI_QKV>(a, s);
+    case EPI_RESID: return launch_v<T, MT, NT, EPI_RESID>(a, s);
+    case EPI_SWIGLU: return launch_v<T, MT, NT < 2 ? 2 : NT, EPI_SWIGLU>(a, s);
+    default: return launch_v<T, MT, NT, EPI_LOGITS>(a, s);
+  }
+}
+
+// mt = 16-row tiles of the step's rows (up to 8 in the bf16 mode, 4 in the
+// f32 mode); nt = 16-column tiles per workgroup (gemm_tiles).
+template <typename T, int MT>
+static hipError_t launch_rows(int epi, int nt, const GemmArgs& a, hipStream_t s) {
+  switch (nt) {
+    case 1: return launch_mt<T, MT, 1>(epi, a, s);
+    case 2: return launch_mt<T, MT, 2>(epi, a, s);
+    case 4: return launch_mt<T, MT, 4>(epi, a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gemm(bool bf16, int epi, int mt, int nt, const GemmArgs& a, hipStream_t s) {
+  if (nt != gemm_tiles(epi, mt, a.N)) return hipErrorInvalidValue;
   if (bf16) {
     switch (mt) {
-      case 1: return launch_mt<__bf16, 1>(epi, a, s);
-      case 2: return launch_mt<__bf16, 2>(epi, a, s);
-      case 3: return launch_mt<__bf16, 3>(epi, a, s);
-      case 4: return launch_mt<__bf16, 4>(epi, a, s);
-      case 5: return launch_mt<__bf16, 5>(epi, a, s);
-      case 6: return launch_mt<__bf16, 6>(epi, a, s);
-      case 7: return launch_mt<__bf16, 7>(epi, a, s);
-      case 8: return launch_mt<__bf16, 8>(epi, a, s);
+      case 1: return launch_rows<__bf16, 1>(epi, nt, a, s);
+      case 2: return launch_rows<__bf16, 2>(epi, nt, a, s);
+      case 3: return launch_rows<__bf16, 3>(epi, nt, a, s);
+      case 4: return launch_rows<__bf16, 4>(epi, nt, a, s);
+      case 5: return launch_rows<__bf16, 5>(epi, nt, a, s);
+      case 6: return launch_rows<__bf16, 6>(epi, nt, a, s);
+      case 7: return launch_rows<__bf16, 7>(epi, nt, a, s);
+      case 8: return launch_rows<__bf16, 8>(epi, nt, a, s);
       default: return hipErrorInvalidValue;
     }
   }
   switch (mt) {
-    case 1: return launch_mt<float, 1>(epi, a, s);
-    case 2: return launch_mt<float, 2>(epi, a, s);
-    case 3: return launch_mt<float, 3>(epi, a, s);
-    case 4: return launch_mt<float, 4>(epi, a, s);
+    case 1: return launch_rows<float, 1>(epi, nt, a, s);
+    case 2: return launch_rows<float, 2>(epi, nt, a, s);
+    case 3: return launch_rows<float, 3>(epi, nt, a, s);
+    case 4: return launch_rows<float, 4>(epi, nt, a, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -644,6 +644,7 @@ struct ProfScope {
 
 EmbedArgs embed_args(tss_ctx* c);
 
+
 // Layer after `l` that sequence i runs (n_layers = none), and the gain of the
 // RMSNorm that layer (or the final norm) applies first.
 int next_active(const tss_ctx* c, int i, int l) {
@@ -749,7 +750,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
       a.head_dim = hd;
       a.d = d;
       ProfScope ps(c, TSS_K_QKV, l);
-      HIPCHK(launch_gemm(c->bf16, EPI_QKV, mt, a, s), "qkv gemm");
+      HIPCHK(launch_gemm(c->bf16, EPI_QKV, mt, gemm_tiles(EPI_QKV, mt, a.N), a, s), "qkv gemm");
       ps.done();
     }
     {  // tree attention
@@ -790,7 +791,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
       for (int i = 0; i < kMaxBatch; ++i) a.g_next[i] = (const float*)(c->w + W.mlp_norm);
       a.ss_out = (float*)(ws + c->wsl.ss_m);
       ProfScope ps(c, TSS_K_OPROJ, l);
-      HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, a, s), "o gemm");
+      HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, gemm_tiles(EPI_RESID, mt, a.N), a, s), "o gemm");
       ps.done();
     }
     {  // RMSNorm + gate/up + SwiGLU
@@ -805,7 +806,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
       a.act = ws + c->wsl.act;
       a.act_plane = plane_f;
       ProfScope ps(c, TSS_K_GATEUP, l);
-      HIPCHK(launch_gemm(c->bf16, EPI_SWIGLU, mt, a, s), "gate/up gemm");
+      HIPCHK(launch_gemm(c->bf16, EPI_SWIGLU, mt, gemm_tiles(EPI_SWIGLU, mt, a.N), a, s), "gate/up gemm");
       ps.done();
     }
     {  // down projection + residual; next norm input (each sequence's next block, or the final norm)
@@ -822,7 +823,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
       for (int i = 0; i < kMaxBatch; ++i) a.g_next[i] = attn_gain_of(c, i < B ? next_active(c, i, l) : L);
       a.ss_out = (float*)(ws + c->wsl.ss_a);
       ProfScope ps(c, TSS_K_DOWN, l);
-      HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, a, s), "down gemm");
+      HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, gemm_tiles(EPI_RESID, mt, a.N), a, s), "down gemm");
       ps.done();
     }
   }
@@ -841,7 +842,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
       a.am_val = (float*)(ws + c->wsl.am_val);
       a.am_idx = (int32_t*)(ws + c->wsl.am_idx);
       ProfScope ps(c, TSS_K_LMHEAD, -1);
-      HIPCHK(launch_gemm(c->bf16, EPI_LOGITS, mt, a, s), "lm_head gemm");
+      HIPCHK(launch_gemm(c->bf16, EPI_LOGITS, mt, gemm_tiles(EPI_LOGITS, mt, a.N), a, s), "lm_head gemm");
       ps.done();
     }
     {

@@ -244,7 +244,7 @@ LaunchTiming& launch_timing();
   } while (0)
 
 // Launchers (defined in the .hip files).  T is selected by `bf16`.
-hipError_t launch_gemm(bool bf16, int epi, int mt, const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm(bool bf16, int epi, int mt, int nt, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attn(bool bf16, int head_dim, int max_tiles, int n_seq, const AttnArgs& a, hipStream_t s);
 hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
@@ -254,9 +254,24 @@ hipError_t init_kernel_attributes();  // attention
 hipError_t init_gemm_attributes();
 hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base, hipStream_t s);
 
-// Strip width (16-row tiles per strip) of a packed matrix: gate and up tiles
-// pair up so one workgroup sees both halves of SwiGLU; every other matrix
-// uses single-tile strips.
-inline int strip_tiles(int epi) { return epi == EPI_SWIGLU ? 2 : 1; }
+// 16-column tiles per workgroup of a projection launch.  A workgroup streams
+// its tiles over all of K, so every workgroup reads all of the step's
+// activation tiles: a wider block makes each activation tile serve more
+// weight tiles, but leaves fewer workgroups.  Measured on the 7B, 13B and
+// 33B shapes (6 to 72 rows): the best width is the narrowest that fits the
+// matrix in one round of at most 256 workgroups (with more than one row tile
+// a workgroup fills a CU), except that with one row tile gate/up keeps one
+// gate/up pair, lm_head one tile, and Q/K/V takes 4 tiles only if that fits
+// 256 workgroups (else 2).  (Splitting K over workgroups to widen the blocks
+// further measured slower: partial sums and a device-scope fence per
+// workgroup.)
+inline int gemm_tiles(int epi, int mt, int N) {
+  if (epi == EPI_SWIGLU) return (mt == 1 || N % 64) ? 2 : 4;
+  if (mt == 1 && epi == EPI_LOGITS) return 1;
+  if (mt == 1 && epi == EPI_QKV) return (N % 64 == 0 && N / 64 <= 256) ? 4 : (N % 32 == 0 ? 2 : 1);
+  for (int nt = 1; nt <= 4; nt *= 2)
+    if (N % (16 * nt) == 0 && N / (16 * nt) <= 256) return nt;
+  return N % 64 == 0 ? 4 : (N % 32 == 0 ? 2 : 1);
+}
 
 }  // namespace tss
