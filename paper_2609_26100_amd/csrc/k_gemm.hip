@@ -65,11 +65,12 @@ __device__ __forceinline__ uint4 load_stream(const uint8_t* p) {
 // Chunks each wave keeps in flight: a ring of D slots, each holding one
 // chunk's weight tiles (NT x 4 VGPRs) and activation tiles (MT x S x 4
 // VGPRs), sized to about 160 VGPRs per lane.
-// (64 VGPRs with one row tile, where more would cost occupancy; 128 above;
+// (64 VGPRs with one row tile, where more would cost occupancy, and with the
+// largest accumulator sets (20+ tiles), where more would spill; 128 between;
 // measured on the 7B projections)
 template <int MT, int NT, int S> struct Depth {
   static constexpr int per = NT * 4 + MT * S * 4;
-  static constexpr int raw = (MT == 1 ? 64 : 128) / per;
+  static constexpr int raw = (MT == 1 || MT * NT >= 20 ? 64 : 128) / per;
   static constexpr int v = raw < 1 ? 1 : (raw > 8 ? 8 : raw);
 };
 
