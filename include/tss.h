@@ -195,6 +195,30 @@ int tss_verify_batch(tss_ctx* ctx, int32_t n_seqs, const int32_t* seq_ids, const
                      const int32_t* draft_tokens, const int32_t* tree_parents, const uint8_t* skip_masks,
                      uint32_t flags, int32_t* accept_len, int32_t* next_token);
 
+/* Verifies one draft tree of one sequence under n_masks skip masks, without
+ * committing: the candidate evaluations of the offline skip-set search
+ * (Acceptance- and Metric-Aware Breadth Search, Algorithm 1, which evaluates
+ * the dense baseline, every single-layer skip and every subset of the
+ * candidate pool at each search depth on the same calibration input).
+ * Results equal n_masks calls of tss_verify(seq, draft, parent, n_nodes,
+ * mask_k, 0, ...) up to floating-point summation order.
+ *   skip_masks: n_masks * n_layers bytes, mask k at k * n_layers.  Every layer
+ *     any mask runs must hold K/V for the committed context (TSS_ESTATE
+ *     otherwise; prefill the sequence dense for a sweep).
+ *   accept_len[n_masks], next_token[n_masks]: mask k's decision.
+ *   greedy: n_masks * n_nodes greedy tokens (mask k's at k * n_nodes), or NULL.
+ * Consecutive masks are verified together as segments of one step (at most
+ * 32, at most min(max_nodes * max_batch, 128) rows, and only as many as the
+ * sequence's free KV slots hold: each segment writes its draft K/V to its own
+ * slots after the context).  Such a step launches each block that any of its
+ * masks runs once, reading its weights and each context page once for all
+ * of them, so callers should order masks that share skipped layers next to
+ * each other.  The sequence's length and committed K/V are unchanged;
+ * tss_get_logits / tss_get_greedy then return the last step's rows. */
+int tss_verify_sweep(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent,
+                     int32_t n_nodes, int32_t n_masks, const uint8_t* skip_masks, int32_t* accept_len,
+                     int32_t* next_token, int32_t* greedy);
+
 /* Copies the last verify's fp32 logits [n_nodes][vocab] / greedy tokens
  * [n_nodes] to host memory (rows in the step's node order).  n_nodes must not
  * exceed the last verify's node count (all sequences of a batch). */

@@ -1,18 +1,21 @@
 // Tree-masked attention of the verify step over the paged KV cache (gfx950).
 //
-// For every head and node i of a sequence: softmax(q_i K^T / sqrt(hd)) V over
-// the sequence's cached context [0, n_kv) plus its draft nodes visible to i
-// (i itself and its ancestors; their K/V were appended at slots n_kv + j by
-// the QKV kernel).  This is the attention half of an active block; bypassed
-// blocks never reach this kernel (Domain-Aware Skip Controller, block rule).
+// For every head and node i of a segment: softmax(q_i K^T / sqrt(hd)) V over
+// its sequence's cached context [0, n_kv) plus the segment's draft nodes
+// visible to i (i itself and its ancestors; the QKV kernel appended their K/V
+// at the segment's draft slots n_kv + slot0 + j).  This is the attention half
+// of an active block; bypassed blocks never reach this kernel (Domain-Aware
+// Skip Controller, block rule).
 //
-// grid = (head, sequence that runs this block, workgroup of that sequence).
-// A sequence's G workgroups of 8 waves split its pages (wave w of workgroup g
-// walks pages 8 g + w, 8 (g + G) + w, ..., loading the next page while it
-// computes the current one), and each wave applies every page to all of the
-// sequence's node tiles (up to 4 x 16 nodes), so each K/V page is read from
-// HBM once per head however many nodes the tree has.  (Serving the tiles
-// from different waves instead measured slower: more page loads per tile.)
+// grid = (head, item, workgroup of that item).  An item is up to 64
+// consecutive rows of one KV sequence, possibly from several segments (one
+// context verified under several skip masks).  An item's G workgroups of 8
+// waves split the sequence's pages (wave w of workgroup g walks pages
+// 8 g + w, 8 (g + G) + w, ..., loading the next page while it computes the
+// current one), and each wave applies every page to all of the item's row
+// tiles (up to 4 x 16 rows), so each K/V page is read from HBM once per head
+// however many nodes and masks the item carries.  (Serving the tiles from
+// different waves instead measured slower: more page loads per tile.)
 //   * The K page block [16 tokens][hd] is read with one contiguous 64-byte run
 //     per lane (the whole 4 KiB block per wave), and S = K Q^T comes out of
 //     MFMA with tokens on the rows and nodes on the columns.
@@ -31,10 +34,10 @@
 // workgroup order and resets the counter.  No second kernel (a kernel
 // boundary costs about 3 us on this GPU) and bit-reproducible results.
 //
-// A sequence's G (at most `groups`, at least one page per wave, at most
-// pages / (4 T)) is derived on the device from its length, so launch
-// arguments do not depend on context lengths; workgroups beyond a sequence's
-// G exit at once.
+// An item's G (at most `groups`, at least one page per wave, at most
+// pages / (4 T)) is derived on the device from its context length, so launch
+// arguments do not depend on context lengths; workgroups beyond an item's G
+// exit at once.
 #include "tss_internal.h"
 
 namespace tss {
@@ -66,7 +69,7 @@ constexpr size_t attn_lds() {
 
 // TK = KV element type (_Float16 or float); TW = weight type of the mode
 // (selects the activation plane format of the output); TMAX = most node
-// tiles of a sequence in this launch.
+// tiles of an item in this launch.
 template <typename TK, typename TW, int HD, int TMAX>
 __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   constexpr int DL = HD / 4;                         // dims per lane group in Q K^T
@@ -78,18 +81,18 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 
   const int head = blockIdx.x, y = blockIdx.y, g = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r16 = lane & 15, grp = lane >> 4;
-  const int sq = a.seq_list[y];
+  const int sq = a.item_seg[y];
   const int n_kv = a.sp->seq_nkv[sq];
-  const int row0 = a.sp->seq_row0[sq];
-  const int Ms = a.sp->seq_row0[sq + 1] - row0;      // nodes of the sequence
-  const int T = (Ms + 15) >> 4;                      // its node tiles (<= TMAX)
-  const int n_pages = (n_kv + Ms + kPage - 1) / kPage;
-  // workgroups of this sequence: at most groups, at least a page per wave, and
+  const int row0 = a.item_row0[y];
+  const int Ms = a.item_rows[y];                     // rows of the item
+  const int T = (Ms + 15) >> 4;                      // its row tiles (<= TMAX)
+  const int n_pages = (n_kv + a.item_slots[y] + kPage - 1) / kPage;
+  // workgroups of this item: at most groups, at least a page per wave, and
   // few enough that partial states (T tiles each) stay well below the pages
   const int G = max(1, min(a.groups, min((n_pages + W - 1) / W, n_pages / (TSS_ATTN_PART_DIV * T))));
   if (g >= G) return;                                // uniform over the workgroup
   const int32_t* pt = a.page_table + a.pt_off[sq];
-  const int arg_pages = sq == 0 ? a.n_arg_pages : 0;
+  const int arg_pages = a.n_arg_pages;
 
   // B operand of S = K Q^T for tile t: lane (node 16 t + r16, group grp)
   // holds q[node][head*HD + grp*DL + 0..DL).  Waves 0..T-1 build one tile
@@ -114,11 +117,16 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       sm_q[(wave * 64 + lane) * NQ + c] = qv;
     }
   }
+  // draft visibility of row (tile t, r16): slot n_kv + base[t] + j holds its
+  // segment's node j, visible when bit j of anc[t] is set
   uint64_t anc[TMAX];
+  int base[TMAX];
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) {
     const int ln = t * 16 + r16;
-    anc[t] = (t < T && ln < Ms) ? a.sp->anc[row0 + ln] : 0ull;
+    const bool in = t < T && ln < Ms;
+    anc[t] = in ? a.sp->anc[row0 + ln] : 0ull;
+    base[t] = in ? (int)a.sp->seg_slot0[a.sp->row_seq[row0 + ln]] : 0;
   }
 
   float m_run[TMAX], l_run[TMAX];
@@ -182,8 +190,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
         if (slot < n_kv) {
           vis = true;
         } else {
-          const int j = slot - n_kv;
-          vis = j < Ms && ((anc[t] >> j) & 1ull);
+          const unsigned j = (unsigned)(slot - n_kv - base[t]);
+          vis = j < 64u && ((anc[t] >> j) & 1ull);
         }
         s[v] = vis ? S[v] * a.scale_log2 : -INFINITY;
         mloc = fmaxf(mloc, s[v]);
@@ -406,10 +414,9 @@ static hipError_t attn_hd(int tiles, int n_seq, const AttnArgs& a, hipStream_t s
   return attn_t<TK, TW, HD, 4>(n_seq, a, s);
 }
 
-// max_tiles = most 16-node tiles of a listed sequence (1..4); n_seq = listed
-// sequences (grid.y).
+// max_tiles = most 16-row tiles of an item (1..4); n_seq = items (grid.y).
 hipError_t launch_attn(bool bf16, int head_dim, int max_tiles, int n_seq, const AttnArgs& a, hipStream_t s) {
-  if (max_tiles < 1 || max_tiles > 4 || n_seq < 1 || n_seq > kMaxBatch) return hipErrorInvalidValue;
+  if (max_tiles < 1 || max_tiles > 4 || n_seq < 1 || n_seq > kAttnMaxItems) return hipErrorInvalidValue;
   if (bf16)
     return head_dim == 128 ? attn_hd<_Float16, __bf16, 128>(max_tiles, n_seq, a, s)
                            : attn_hd<_Float16, __bf16, 64>(max_tiles, n_seq, a, s);

@@ -124,7 +124,8 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       s_seq[r] = sq;
       if constexpr (EPI == EPI_QKV) {
         const int nkv = a.sp->seq_nkv[sq];
-        s_slot[r] = nkv + r - a.sp->seq_row0[sq];  // local node j sits at slot n_kv + j
+        // local node j of segment sq sits at slot n_kv + seg_slot0 + j
+        s_slot[r] = nkv + a.sp->seg_slot0[sq] + r - a.sp->seq_row0[sq];
         s_pos[r] = nkv + a.sp->depth[r];
       }
     }
@@ -304,7 +305,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
         const int sq = s_seq[row];
         const int slot = s_slot[row];
         const int lp = slot >> 4;
-        const int page = (sq == 0 && lp < a.n_arg_pages) ? a.pages[lp] : a.page_table[a.pt_off[sq] + lp];
+        const int page = lp < a.n_arg_pages ? a.pages[lp] : a.page_table[a.pt_off[sq] + lp];
         const int tin = slot & 15;
         KV* blk = (KV*)a.kv_pages +
                   ((((size_t)a.layer * a.n_pages_pool + page) * 2 + (sec - 1)) * a.n_heads + head) * (16 * (size_t)HD);

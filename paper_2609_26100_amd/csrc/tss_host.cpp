@@ -58,16 +58,16 @@ int round16(int x) { return (x + 15) & ~15; }
 int row_cap(const tss_model_cfg* c) {
   return std::min(c->max_nodes * c->max_batch, c->dtype == TSS_BF16 ? kMaxRows : 64);
 }
-// Attention workgroups per (head, sequence) when n_seq sequences run a block:
-// at most about kAttnTargetWGs workgroups in all (at least one per pair).
-int attn_groups(int n_heads, int n_seq) {
-  return std::max(1, std::min(kAttnMaxGroups, kAttnTargetWGs / (n_heads * n_seq)));
+// Attention workgroups per (head, item) when a launch has n_items items: at
+// most about kAttnTargetWGs workgroups in all (at least one per pair).
+int attn_groups(int n_heads, int n_items) {
+  return std::max(1, std::min(kAttnMaxGroups, kAttnTargetWGs / (n_heads * n_items)));
 }
-// partial-state slots of one attention launch: n_heads * n_seq * groups over
-// every n_seq (at most max(kAttnTargetWGs, n_heads * n_seq))
+// partial-state slots of one attention launch: n_heads * n_items * groups
+// over every item count (at most max(kAttnTargetWGs, n_heads * n_items))
 size_t attn_slots(const tss_model_cfg* c) {
   size_t m = 0;
-  for (int n = 1; n <= c->max_batch; ++n) m = std::max(m, (size_t)c->n_heads * n * attn_groups(c->n_heads, n));
+  for (int n = 1; n <= kAttnMaxItems; ++n) m = std::max(m, (size_t)c->n_heads * n * attn_groups(c->n_heads, n));
   return m;
 }
 
@@ -115,7 +115,7 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align256(off + bytes); return o; };
   w.sp = take(sizeof(StepParams));
-  w.result = take(kMaxBatch * sizeof(Result));
+  w.result = take(kMaxSegs * sizeof(Result));
   w.h = take(Mp * d * 4);
   w.xa = take(ap * Mp * d * es);
   w.xm = take(ap * Mp * d * es);
@@ -127,7 +127,7 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   const size_t slots = attn_slots(c);
   w.part_o = take(slots * kAttnMaxTiles * 16 * c->head_dim * 4);
   w.part_ml = take(slots * kAttnMaxTiles * 16 * 2 * 4);
-  w.counters = take((size_t)c->n_heads * kMaxBatch * 4);
+  w.counters = take((size_t)c->n_heads * kAttnMaxItems * 4);
   w.logits = take(Mp * v * 4);
   w.am_val = take((v / 16) * Mp * 4);
   w.am_idx = take((v / 16) * Mp * 4);
@@ -179,15 +179,16 @@ struct tss_ctx {
   hipEvent_t stage_ev[2] = {nullptr, nullptr};
   int stage_cur = 0;
   StepParams* sp_host = nullptr;
-  // the step being enqueued: its sequences, their masks (n_seqs x n_layers)
-  // and which of them need their accepted tree path moved after the commit
+  // the step being enqueued: its segments' KV sequences, their masks
+  // (n_seqs x n_layers) and which of them need their accepted tree path
+  // moved after the commit
   struct Step {
-    int n_seqs = 0;
-    int32_t seq[kMaxBatch] = {};
-    bool compact[kMaxBatch] = {};
+    int n_seqs = 0;  // segments
+    int32_t seq[kMaxSegs] = {};
+    bool compact[kMaxSegs] = {};
     std::vector<uint8_t> mask;
   } step;
-  Result* res_host = nullptr;     // [kMaxBatch] host-mapped, written by the accept kernel
+  Result* res_host = nullptr;     // [kMaxSegs] host-mapped, written by the accept kernel
   Result* res_dev_map = nullptr;  // its device address
   int last_M = 0;
   bool poisoned = false;
@@ -382,11 +383,11 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
   };
   if (e == hipSuccess)
     step("mapped result buffer",
-         hipHostMalloc((void**)&c->res_host, kMaxBatch * sizeof(Result), hipHostMallocMapped | hipHostMallocCoherent));
+         hipHostMalloc((void**)&c->res_host, kMaxSegs * sizeof(Result), hipHostMallocMapped | hipHostMallocCoherent));
   if (e == hipSuccess) step("mapped result address", hipHostGetDevicePointer((void**)&c->res_dev_map, c->res_host, 0));
   if (e == hipSuccess)
     step("attention counters",
-         hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * kMaxBatch * 4, c->stream));
+         hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * kAttnMaxItems * 4, c->stream));
   if (e == hipSuccess) step("stream sync", hipStreamSynchronize(c->stream));
   if (e == hipSuccess) step("attention LDS attribute", init_kernel_attributes());
   if (e == hipSuccess) step("projection LDS attribute", init_gemm_attributes());
@@ -645,7 +646,7 @@ struct ProfScope {
 EmbedArgs embed_args(tss_ctx* c);
 
 
-// Layer after `l` that sequence i runs (n_layers = none), and the gain of the
+// Layer after `l` that segment i runs (n_layers = none), and the gain of the
 // RMSNorm that layer (or the final norm) applies first.
 int next_active(const tss_ctx* c, int i, int l) {
   const int L = c->cfg.n_layers;
@@ -658,15 +659,16 @@ const float* attn_gain_of(const tss_ctx* c, int layer) {
   return (const float*)(c->w + (layer < c->cfg.n_layers ? c->wl.layers[layer].attn_norm : c->wl.final_norm));
 }
 
-// Enqueues embed, the blocks that any sequence of the step runs and (for
+// Enqueues embed, the blocks that any segment of the step runs and (for
 // verify) lm_head + accept (+ KV compaction) for the rows in c->sp_host and
-// the sequences in c->step, on stream s.  A block that every sequence skips
-// is not launched; inside a launched block the rows of sequences that skip it
-// are left untouched (attention does not even list those sequences).  Every
-// kernel argument except the embedding kernel's step parameters depends only
-// on the step's shape (sequences, masks, node counts, compaction), not on
-// context lengths, so a captured sequence of launches can be replayed for
-// later steps of the same shape.
+// the segments in c->step, on stream s.  A block that every segment skips is
+// not launched; inside a launched block the rows of segments that skip it
+// are left untouched (their attention rows, if an item spans them, are
+// computed and discarded).  Every kernel argument except the embedding
+// kernel's step parameters depends only on the step's shape (segments,
+// sequences, masks, node counts, compaction), not on context lengths, so a
+// captured sequence of launches can be replayed for later steps of the same
+// shape.
 int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
   const tss_model_cfg& cf = c->cfg;
   const StepParams& sp = *c->sp_host;
@@ -683,11 +685,15 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
   c->cur_stream = s;
   c->prof_armed = false;
 
-  int32_t pt_off[kMaxBatch] = {};
-  for (int i = 0; i < B; ++i) pt_off[i] = st.seq[i] * pps;
-  // a single sequence's first page ids travel in the kernel arguments
+  int32_t pt_off[kMaxSegs] = {};
+  bool one_seq = true;
+  for (int i = 0; i < B; ++i) {
+    pt_off[i] = st.seq[i] * pps;
+    one_seq = one_seq && st.seq[i] == st.seq[0];
+  }
+  // with one KV sequence in the step its first page ids travel in the kernel arguments
   int32_t arg_pages[kArgPages] = {};
-  const int n_arg_pages = B == 1 ? std::min(pps, kArgPages) : 0;
+  const int n_arg_pages = one_seq ? std::min(pps, kArgPages) : 0;
   for (int i = 0; i < n_arg_pages; ++i) arg_pages[i] = c->pt_host[(size_t)pt_off[0] + i];
 
   {
@@ -712,18 +718,37 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
   base.row_on[0] = base.row_on[1] = ~0ull;
 
   for (int l = 0; l < L; ++l) {
-    // rows and sequences that run block l
+    // rows and segments that run block l; attention items: per KV sequence
+    // (a run of segments with the same sequence), the rows from its first to
+    // its last segment that runs the block, cut into pieces of 64 rows
     uint64_t row_on[kMaxRows / 64] = {0, 0};
     AttnArgs at{};
     int n_act = 0, max_tiles = 1;
-    for (int i = 0; i < B; ++i) {
-      if (st.mask[(size_t)i * L + l]) continue;
-      const int r0 = sp.seq_row0[i], r1 = sp.seq_row0[i + 1];
-      for (int r = r0; r < r1; ++r) row_on[r >> 6] |= 1ull << (r & 63);
-      at.seq_list[n_act++] = (uint8_t)i;
-      max_tiles = std::max(max_tiles, (r1 - r0 + 15) / 16);
+    for (int u0 = 0; u0 < B;) {
+      int u1 = u0 + 1;
+      while (u1 < B && st.seq[u1] == st.seq[u0]) ++u1;
+      int lo = -1, hi = -1;
+      for (int i = u0; i < u1; ++i) {
+        if (st.mask[(size_t)i * L + l]) continue;
+        const int r0 = sp.seq_row0[i], r1 = sp.seq_row0[i + 1];
+        for (int r = r0; r < r1; ++r) row_on[r >> 6] |= 1ull << (r & 63);
+        if (lo < 0) lo = r0;
+        hi = r1;
+      }
+      for (int r = lo; lo >= 0 && r < hi; r += 4 * 16) {
+        if (n_act == kAttnMaxItems) return fail(c, TSS_EINVAL, "too many attention items in one step");
+        const int rows = std::min(64, hi - r);
+        const int last_seg = sp.row_seq[r + rows - 1];
+        at.item_row0[n_act] = (uint8_t)r;
+        at.item_rows[n_act] = (uint8_t)rows;
+        at.item_seg[n_act] = sp.row_seq[r];
+        at.item_slots[n_act] = (uint8_t)(sp.seg_slot0[last_seg] + sp.seq_row0[last_seg + 1] - sp.seq_row0[last_seg]);
+        max_tiles = std::max(max_tiles, (rows + 15) / 16);
+        ++n_act;
+      }
+      u0 = u1;
     }
-    if (n_act == 0) continue;  // every sequence skips this block
+    if (n_act == 0) continue;  // every segment skips this block
     const LayerW& W = c->wl.layers[l];
     GemmArgs lb = base;
     lb.row_on[0] = row_on[0];
@@ -788,7 +813,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
       a.h = (float*)(ws + c->wsl.h);
       a.xn = ws + c->wsl.xm;
       a.xn_plane = plane_d;
-      for (int i = 0; i < kMaxBatch; ++i) a.g_next[i] = (const float*)(c->w + W.mlp_norm);
+      for (int i = 0; i < kMaxSegs; ++i) a.g_next[i] = (const float*)(c->w + W.mlp_norm);
       a.ss_out = (float*)(ws + c->wsl.ss_m);
       ProfScope ps(c, TSS_K_OPROJ, l);
       HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, gemm_tiles(EPI_RESID, mt, a.N), a, s), "o gemm");
@@ -820,7 +845,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
       a.h = (float*)(ws + c->wsl.h);
       a.xn = ws + c->wsl.xa;
       a.xn_plane = plane_d;
-      for (int i = 0; i < kMaxBatch; ++i) a.g_next[i] = attn_gain_of(c, i < B ? next_active(c, i, l) : L);
+      for (int i = 0; i < kMaxSegs; ++i) a.g_next[i] = attn_gain_of(c, i < B ? next_active(c, i, l) : L);
       a.ss_out = (float*)(ws + c->wsl.ss_a);
       ProfScope ps(c, TSS_K_DOWN, l);
       HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, gemm_tiles(EPI_RESID, mt, a.N), a, s), "down gemm");
@@ -915,7 +940,7 @@ EmbedArgs embed_args(tss_ctx* c) {
   a.embed = c->w + c->wl.embed;
   a.sp = sp;
   a.sp_dev = (StepParams*)(c->ws + c->wsl.sp);
-  for (int i = 0; i < kMaxBatch; ++i) a.gain[i] = attn_gain_of(c, i < c->step.n_seqs ? next_active(c, i, -1) : 0);
+  for (int i = 0; i < kMaxSegs; ++i) a.gain[i] = attn_gain_of(c, i < c->step.n_seqs ? next_active(c, i, -1) : 0);
   a.h = (float*)(c->ws + c->wsl.h);
   a.xn = c->ws + c->wsl.xa;
   a.xn_plane = act_planes(&cf) == 2 ? (size_t)c->Mp * cf.d_model : 0;
@@ -1102,9 +1127,85 @@ int verify_batch(tss_ctx* c, int32_t n_seqs, const int32_t* seq_ids, const int32
   return TSS_OK;
 }
 
+// One draft tree of one sequence verified under many skip masks (dry runs):
+// consecutive masks are packed into steps of several segments that share the
+// sequence's context (each segment takes its own draft slots after it), so a
+// step reads each launched block's weights and each context page once for
+// all of its masks.  Direct launches: sweep steps rarely repeat a shape, and
+// capturing each would cost more than it saves and evict the decode steps'
+// graphs.
+int verify_sweep(tss_ctx* c, int32_t seq, const int32_t* tokens, const int32_t* parent, int32_t n,
+                 int32_t n_masks, const uint8_t* masks, int32_t* accept_len, int32_t* next_token, int32_t* greedy) {
+  int r = check_ready(c, seq);
+  if (r) return r;
+  if (!tokens || !masks || !accept_len || !next_token) return fail(c, TSS_EINVAL, "null argument");
+  if (n_masks < 1) return fail(c, TSS_EINVAL, "n_masks must be at least 1");
+  if (validate_tree(parent, n, c->cfg.max_nodes) != TSS_OK)
+    return fail(c, TSS_EINVAL, "invalid draft tree (n_nodes, parent[0] = -1, 0 <= parent[i] < i)");
+  for (int j = 0; j < n; ++j)
+    if (tokens[j] < 0 || tokens[j] >= c->cfg.vocab) return fail(c, TSS_EINVAL, "token outside [0, vocab)");
+  const int L = c->cfg.n_layers;
+  if (!mask_ok(masks, n_masks * L)) return fail(c, TSS_EINVAL, "mask bytes must be 0 or 1");
+  if (c->n_kv[seq] + n > c->max_tokens) return fail(c, TSS_ECAPACITY, "verify exceeds the sequence's KV capacity");
+  for (int k = 0; k < n_masks; ++k)
+    for (int l = 0; l < L; ++l)
+      if (!masks[(size_t)k * L + l] && c->kv_len[seq][l] != c->n_kv[seq])
+        return fail(c, TSS_ESTATE, "an active layer lacks K/V for the committed context");
+  // masks per step: segment limit, row capacity, draft slots left in the sequence
+  const int per_step = std::min({kMaxSegs, row_cap(&c->cfg) / n, (c->max_tokens - c->n_kv[seq]) / n});
+  int32_t depth[kMaxNodes];
+  uint64_t anc[kMaxNodes];
+  tree_meta(parent, n, depth, anc);
+  tss_ctx::Step& st = c->step;
+  for (int k0 = 0; k0 < n_masks; k0 += per_step) {
+    const int P = std::min(per_step, n_masks - k0);
+    StepParams& sp = *c->sp_host;
+    std::memset(&sp, 0, sizeof(sp));
+    sp.M = P * n;
+    sp.n_seqs = P;
+    st.n_seqs = P;
+    st.mask.assign(masks + (size_t)k0 * L, masks + (size_t)(k0 + P) * L);
+    for (int i = 0; i < P; ++i) {
+      const int r0 = i * n;
+      st.seq[i] = seq;
+      st.compact[i] = false;
+      sp.seq_row0[i] = r0;
+      sp.seq_nkv[i] = c->n_kv[seq];
+      sp.seg_slot0[i] = (uint8_t)r0;
+      for (int j = 0; j < n; ++j) {
+        sp.tok[r0 + j] = tokens[j];
+        sp.parent[r0 + j] = (int8_t)(parent ? parent[j] : j - 1);
+        sp.depth[r0 + j] = (uint8_t)depth[j];
+        sp.anc[r0 + j] = anc[j];
+        sp.row_seq[r0 + j] = (uint8_t)i;
+      }
+    }
+    sp.seq_row0[P] = P * n;
+    r = run_step(c, true);
+    if (r) return r;
+    c->last_M = P * n;
+    for (int i = 0; i < P; ++i) {
+      accept_len[k0 + i] = c->res_host[i].accept_len;
+      next_token[k0 + i] = c->res_host[i].next_token;
+    }
+    if (greedy)
+      HIPCHK(hipMemcpy(greedy + (size_t)k0 * n, c->ws + c->wsl.greedy, (size_t)P * n * 4, hipMemcpyDeviceToHost),
+             "greedy copy");
+  }
+  return TSS_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int tss_verify_sweep(tss_ctx* c, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent,
+                     int32_t n_nodes, int32_t n_masks, const uint8_t* skip_masks, int32_t* accept_len,
+                     int32_t* next_token, int32_t* greedy) {
+  if (!c) return TSS_EINVAL;
+  return verify_sweep(c, seq, draft_tokens, tree_parent, n_nodes, n_masks, skip_masks, accept_len, next_token,
+                      greedy);
+}
 
 int tss_prefill(tss_ctx* c, int32_t seq, const int32_t* tokens, int32_t n) {
   if (!c) return TSS_EINVAL;

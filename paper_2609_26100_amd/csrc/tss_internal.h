@@ -45,12 +45,14 @@ namespace tss {
 
 constexpr int kPage = 16;          // tokens per KV page
 constexpr int kMaxNodes = 64;      // nodes of one sequence in one step (u64 ancestor masks)
-constexpr int kMaxBatch = 8;       // sequences of one step
-constexpr int kMaxRows = 128;      // rows (nodes of every sequence) of one step
+constexpr int kMaxBatch = 8;       // KV sequences of one step
+constexpr int kMaxSegs = 32;       // segments (node sets with their own skip mask) of one step
+constexpr int kMaxRows = 128;      // rows (nodes of every segment) of one step
 constexpr int kMaxLayers = 256;
 constexpr int kTileBytes = 1024;   // one packed 16 x KC weight tile
 constexpr int kAttnMaxGroups = 16; // workgroups per (head, sequence) in attention
-constexpr int kAttnMaxTiles = 4;   // 16-node tiles of one sequence in attention (kMaxNodes / 16)
+constexpr int kAttnMaxTiles = 4;   // 16-row tiles of one attention item (64 rows)
+constexpr int kAttnMaxItems = 16;  // attention items (row ranges of one KV sequence) of one launch
 // attention workgroups one launch aims for: one round, a little under one
 // per CU (measured best on the 7B, 13B and 33B shapes)
 #ifndef TSS_ATTN_TARGET_WGS
@@ -94,18 +96,24 @@ __device__ __forceinline__ void store_act(void* base, size_t plane, size_t idx, 
 }
 
 // Per-step data that changes from step to step (tokens, tree, context
-// lengths).  Rows are the nodes of every sequence of the step, sequence after
-// sequence; a sequence's nodes are numbered locally from 0 (its root).
+// lengths).  Rows are grouped into segments: the nodes of one draft tree
+// verified under one skip mask, numbered locally from 0 (its root), segment
+// after segment.  A segment belongs to one KV sequence; several segments of
+// one sequence (one context verified under several masks) sit next to each
+// other and take consecutive draft slots after the context: node j of
+// segment s has slot seq_nkv[s] + seg_slot0[s] + j.  In a plain batch every
+// segment is its own sequence and seg_slot0 is 0.
 struct StepParams {
   int32_t M;                       // rows
-  int32_t n_seqs;
-  int32_t seq_row0[kMaxBatch + 1]; // first row of each sequence; seq_row0[n_seqs] = M
-  int32_t seq_nkv[kMaxBatch];      // committed context length of each sequence
+  int32_t n_seqs;                  // segments
+  int32_t seq_row0[kMaxSegs + 1];  // first row of each segment; seq_row0[n_seqs] = M
+  int32_t seq_nkv[kMaxSegs];       // committed context length of each segment's sequence
   int32_t tok[kMaxRows];
   uint64_t anc[kMaxRows];          // bit j: local node j is this node or one of its ancestors
   int8_t parent[kMaxRows];         // local parent (-1 for the root)
   uint8_t depth[kMaxRows];
-  uint8_t row_seq[kMaxRows];       // sequence (0 .. n_seqs-1) of the row
+  uint8_t row_seq[kMaxRows];       // segment (0 .. n_seqs-1) of the row
+  uint8_t seg_slot0[kMaxSegs];     // first draft slot of each segment, after its sequence's context
 };
 
 // Position of a row: its sequence's committed length plus its depth.
@@ -138,24 +146,24 @@ struct GemmArgs {
   float eps;
   int Mp;                  // row stride of the partial-sum arrays
   const StepParams* sp;
-  // rows whose sequence runs this block (bit r of row_on[r / 64]); the QKV
+  // rows whose segment runs this block (bit r of row_on[r / 64]); the QKV
   // and residual epilogues write nothing for the other rows
   uint64_t row_on[kMaxRows / 64];
-  int n_seqs;
+  int n_seqs;              // segments
   // EPI_QKV
   float* q;                // [Mp][d]
   uint8_t* kv_pages;       // first page of the pool
-  const int32_t* page_table;  // the pool's page table; sequence s's pages start at pt_off[s]
-  int32_t pt_off[kMaxBatch];
-  int32_t n_arg_pages;     // with one sequence: valid entries of pages[]
-  int32_t pages[kArgPages];  // physical ids of the first pages of a single sequence
+  const int32_t* page_table;  // the pool's page table; segment s's sequence's pages start at pt_off[s]
+  int32_t pt_off[kMaxSegs];
+  int32_t n_arg_pages;     // with one KV sequence in the step: valid entries of pages[] (else 0)
+  int32_t pages[kArgPages];  // physical ids of that sequence's first pages
   const float2* rope;      // [max_pos][hd/2] (cos, sin)
   int layer, n_pages_pool, n_heads, head_dim, d;
   // EPI_RESID
   float* h;                // [Mp][N] residual, updated in place
   void* xn;                // [Mp][N] activation planes of h_new * g_next
   size_t xn_plane;
-  const float* g_next[kMaxBatch];  // gain of each sequence's next RMSNorm
+  const float* g_next[kMaxSegs];   // gain of each segment's next RMSNorm
   float* ss_out;           // [M][ss_stride] partial sums of h_new^2, one per strip
   // EPI_SWIGLU
   void* act;               // [Mp][N/2] activation planes of silu(gate) * up
@@ -167,6 +175,9 @@ struct GemmArgs {
   int am_stride;
 };
 
+// An attention item is a range of at most 64 consecutive rows of one KV
+// sequence (grid.y walks the items): its workgroups read the sequence's pages
+// once for all of its rows, whatever segments they belong to.
 struct AttnArgs {
   const float* q;          // [Mp][d] row-major
   const uint8_t* kv_pages;
@@ -174,24 +185,27 @@ struct AttnArgs {
   const StepParams* sp;
   void* o;                 // activation planes of the attention output (act_index order)
   size_t o_plane;
-  // partial states, slot ((head * n_seq + y) * groups + g), kAttnMaxTiles tiles each
+  // partial states, slot ((head * n_items + y) * groups + g), kAttnMaxTiles tiles each
   float* part_o;           // [slots][kAttnMaxTiles][16][hd] unnormalised partial outputs
   float* part_ml;          // [slots][kAttnMaxTiles][16][2] (max in log2 units, sum)
-  int* counters;           // [H * kMaxBatch] arrivals, zero between launches
-  int groups;              // most workgroups per (head, sequence)
+  int* counters;           // [H * kAttnMaxItems] arrivals, zero between launches
+  int groups;              // most workgroups per (head, item)
   int layer, n_pages_pool, n_heads, d;
   float scale_log2;        // log2(e) / sqrt(hd)
-  uint8_t seq_list[kMaxBatch];  // grid.y -> sequence (those that run this block)
-  int32_t pt_off[kMaxBatch];
-  int32_t n_arg_pages;     // with one sequence: valid entries of pages[]
-  int32_t pages[kArgPages];  // physical ids of the first pages of a single sequence
+  uint8_t item_row0[kAttnMaxItems];   // first row of the item
+  uint8_t item_rows[kAttnMaxItems];   // rows (1 .. 64)
+  uint8_t item_seg[kAttnMaxItems];    // segment of the first row (context length, page table)
+  uint8_t item_slots[kAttnMaxItems];  // draft slots after the context that its rows may see
+  int32_t pt_off[kMaxSegs];
+  int32_t n_arg_pages;     // with one KV sequence in the step: valid entries of pages[] (else 0)
+  int32_t pages[kArgPages];  // physical ids of that sequence's first pages
 };
 
 struct EmbedArgs {
   const void* embed;       // [V][d] T
   StepParams sp;           // this step's parameters (by value) ...
   StepParams* sp_dev;      // ... copied here for the later kernels of the step
-  const float* gain[kMaxBatch];  // per sequence: gain of the first RMSNorm its rows meet
+  const float* gain[kMaxSegs];   // per segment: gain of the first RMSNorm its rows meet
   float* h;                // [Mp][d]
   void* xn;                // [Mp][d] activation planes
   size_t xn_plane;
@@ -206,7 +220,7 @@ struct AcceptArgs {
   int nparts, M, am_stride;
   const StepParams* sp;
   int32_t* greedy;         // [Mp]
-  Result* result;          // [n_seqs] device copy (read by the compaction kernel)
+  Result* result;          // [n_seqs] device copy, one per segment (read by the compaction kernel)
   Result* result_host;     // [n_seqs] host-mapped pinned copy (read by the host after the step)
 };
 
@@ -245,7 +259,7 @@ LaunchTiming& launch_timing();
 
 // Launchers (defined in the .hip files).  T is selected by `bf16`.
 hipError_t launch_gemm(bool bf16, int epi, int mt, int nt, const GemmArgs& a, hipStream_t s);
-hipError_t launch_attn(bool bf16, int head_dim, int max_tiles, int n_seq, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn(bool bf16, int head_dim, int max_tiles, int n_items, const AttnArgs& a, hipStream_t s);
 hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_compact(bool bf16, int n_seqs, const CompactArgs& a, hipStream_t s);

@@ -75,6 +75,12 @@ class Verifier:
             assert m.size == L * len(seqs)
         return abi.tss_verify_batch(self.ctx, seqs, tokens, offs, par, m, abi.TSS_COMMIT if commit else 0)
 
+    def verify_sweep(self, seq, tokens, masks, parent=None, want_greedy=False):
+        """Dry runs of one draft tree under each mask (rows of masks); returns
+        (accept_len[k], next_token[k]) and, with want_greedy, greedy[k][n]."""
+        m = np.asarray(masks, dtype=np.uint8).reshape(-1, self.shape.n_layers)
+        return abi.tss_verify_sweep(self.ctx, seq, tokens, parent, m, want_greedy)
+
     def logits(self, n_nodes):
         return abi.tss_get_logits(self.ctx, n_nodes, self.shape.vocab)
 
