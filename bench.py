@@ -336,7 +336,7 @@ def workload_sweep_33b(args):
     from 2-59 verified back to back as dry runs (timing only)."""
     shape = synth.LLAMA_33B
     ctx_n = 4096
-    v = _load_verifier(shape, n_seqs=1, max_tokens=ctx_n + 40, max_nodes=33)
+    v = _load_verifier(shape, n_seqs=1, max_tokens=ctx_n + 112, max_nodes=33, max_batch=4)
     toks = synth.context_tokens(shape.vocab, ctx_n + 1, stream=5)
     v.prefill(0, toks[:ctx_n])
     parent = synth.topk_tree_parents((4, 3, 2, 1, 1), (4, 10, 10, 5, 3))
@@ -367,6 +367,13 @@ def workload_sweep_33b(args):
         lat_all.append(lat)
         acc_all.append(acc)
         by_all.append(by)
+    all_masks = np.stack(masks)
+    v.verify_sweep(0, tokens, all_masks, parent)
+    t0 = time.perf_counter()
+    for _ in range(n_steps):
+        v.verify_sweep(0, tokens, all_masks, parent)
+    packed = (time.perf_counter() - t0) / n_steps
+    log(f"33B sweep: 64 masks packed {packed * 1e3:.1f} ms vs {sum(p[1] for p in per_mask) / 1e3:.1f} ms one by one")
     sk = np.array([p[0] for p in per_mask], float)
     us = np.array([p[1] for p in per_mask])
     slope, icpt = np.polyfit(sk, us, 1)
@@ -381,7 +388,166 @@ def workload_sweep_33b(args):
            "us_per_skipped_layer": float(-slope), "us_at_zero_skips_fit": float(icpt),
            "roofline_us_per_skipped_layer": batch_bytes(shape, [(np.zeros(shape.n_layers), ctx_n, 33)]) / PEAK_HBM * 1e6
            - batch_bytes(shape, [(synth.mask_from_layers(shape.n_layers, [2]), ctx_n, 33)]) / PEAK_HBM * 1e6,
-           "per_mask": [{"skipped": p[0], "latency_us": p[1], "roofline_frac": p[2]} for p in per_mask]}
+           "per_mask": [{"skipped": p[0], "latency_us": p[1], "roofline_frac": p[2]} for p in per_mask],
+           "packed_sweep_ms": packed * 1e3, "one_by_one_ms": sum(p[1] for p in per_mask) / 1e3,
+           "packed_speedup": sum(p[1] for p in per_mask) / 1e6 / packed}
+    _free(v)
+    return out
+
+
+def workload_decode_7b(args, v):
+    """7B, 1024-token prompt, T = 96 new tokens (the paper's decoding length):
+    plain autoregressive greedy decoding (one verify per token) against
+    speculative decoding with a synthetic drafter that follows the reference
+    continuation with p = 0.8 (chain k = 5, and the 60-node top-k tree), dense
+    and with 4 layers skipped.  Wall time of the whole loop, host included."""
+    from paper_2609_26100_amd.decode import autoregressive_decode, speculative_decode
+    shape = synth.LLAMA_7B
+    T, ctx_n = 96, CTX
+    prompt = synth.context_tokens(shape.vocab, ctx_n + 1, stream=9)
+    tree = synth.topk_tree_parents((4, 3, 2, 2, 1, 1), (4, 12, 20, 12, 8, 4))
+    out = {"workload": "7B-shape, 1024-token prompt, 96 new tokens, synthetic drafter p=0.8", "T": T, "runs": {}}
+    for skip in (0, 4):
+        mask = synth.nested_skip_masks(shape.n_layers, 16, 31, [skip], stream=1)[skip]
+        v.truncate(0, 0)
+        v.set_mask(0, mask)
+        v.prefill(0, prompt[:ctx_n])
+        base = ctx_n
+        autoregressive_decode(v, 0, int(prompt[ctx_n]), 8)      # capture the one-node step
+        v.truncate(0, base)
+        ref = autoregressive_decode(v, 0, int(prompt[ctx_n]), T)
+        runs = {"autoregressive": ref}
+        for name, drafter in [("chain_k5", synth.ReferenceDrafter(ref.tokens, shape.vocab, 0.8, k=5, stream=11)),
+                              ("tree60", synth.ReferenceDrafter(ref.tokens, shape.vocab, 0.8, parent=tree, stream=12))]:
+            v.truncate(0, base)
+            speculative_decode(v, 0, int(prompt[ctx_n]), 16, drafter)  # capture the step shapes
+            v.truncate(0, base)
+            drafter.rng = np.random.default_rng(1000 + skip)
+            runs[name] = speculative_decode(v, 0, int(prompt[ctx_n]), T, drafter)
+        for name, r in runs.items():
+            same = int(np.sum(np.cumprod(r.tokens == ref.tokens)))
+            out["runs"][f"skip{skip}_{name}"] = {
+                "tok_s": r.tokens_per_second, "steps": r.steps, "tokens_per_step": r.tokens_per_step,
+                "ms": r.seconds * 1e3, "draft_ms": r.draft_seconds * 1e3, "equal_prefix": same,
+                "speedup_vs_autoregressive": ref.seconds / r.seconds}
+            log(f"decode skip {skip} {name}: {r.tokens_per_second:.0f} tok/s, {r.steps} steps, "
+                f"{r.tokens_per_step:.2f} tokens/step, equal to autoregressive for {same}/{T}")
+    v.truncate(0, 0)
+    v.set_mask(0, None)
+    best = out["runs"]["skip0_chain_k5"]
+    out["latency_us_median"] = best["ms"] * 1e3 / best["steps"]
+    out["accepted_tok_s"] = best["tok_s"]
+    return out
+
+
+def workload_search_7b(args):
+    """Algorithm 1 on the 7B shape: 8 calibration items (512-token contexts,
+    chain k = 5 drafts that follow, with p = 0.9, the greedy tokens of the
+    verifier with a hidden set of 4 layers from 16-31 skipped, a stand-in for a
+    drafter aligned with a shallower verifier).  Acceptance and the metric
+    stand-in come from packed mask sweeps, the cost from timed single verifies
+    of the feasible sets.  The task metric is not available here: its stand-in
+    is reported but its tolerance is left open (eps_M = 100 %), so feasibility
+    is decided by acceptance (within 5 % of dense).  Also times the sweep
+    against one verify per mask."""
+    from paper_2609_26100_amd.search import MeasuredCost, SweepQuality, breadth_search
+    shape = synth.LLAMA_7B
+    n_items, ctx_n, k = 8, 512, 5
+    v = _load_verifier(shape, n_seqs=n_items, max_tokens=ctx_n + 130, max_nodes=64, max_batch=8)
+    hidden = synth.random_skip_mask(shape.n_layers, 16, 31, 4, stream=77)
+    items = []
+    for i in range(n_items):
+        toks = synth.context_tokens(shape.vocab, ctx_n + 1, stream=700 + i)
+        v.prefill(i, toks[:ctx_n])
+        cur = [int(toks[ctx_n])]
+        for _ in range(k):
+            v.verify(i, cur, mask=hidden)
+            cur.append(int(v.greedy(len(cur))[-1]))
+        d = np.concatenate([[cur[0]], synth.chain_draft(np.asarray(cur[1:]), shape.vocab, p_accept=0.9,
+                                                        stream=800 + i)])
+        items.append((i, d.astype(np.int32), None))
+    quality = SweepQuality(v, items)
+    cost = MeasuredCost(v, items[0], reps=5)
+    lines = []
+    res = breadth_search(shape.n_layers, 4, quality, cost, eps_A=0.05, eps_M=1.0, tau_A=0.0, tau_M=0.0,
+                         relative=True, log=lines.append)
+    for ln in lines:
+        log("search: " + ln)
+    # sweep throughput: 64 masks of 1-4 layers from 16-31, packed vs one verify per mask
+    rng = np.random.default_rng(5)
+    masks = np.stack([synth.random_skip_mask(shape.n_layers, 16, 31, int(rng.integers(1, 5)), stream=900 + j)
+                      for j in range(64)])
+    seq, tok, _ = items[0]
+    v.verify_sweep(seq, tok, masks)
+    t0 = time.perf_counter()
+    reps = 5
+    for _ in range(reps):
+        v.verify_sweep(seq, tok, masks)
+    packed = (time.perf_counter() - t0) / reps
+    for mk in masks:
+        v.verify(seq, tok, mask=mk)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        for mk in masks:
+            v.verify(seq, tok, mask=mk)
+    single = (time.perf_counter() - t0) / reps
+    cfg = res.config(shape.n_layers)
+    out = {"workload": "7B-shape breadth search (Algorithm 1), 8 calibration items, chain k=5, 512-token contexts",
+           "hidden_skip": np.nonzero(hidden)[0].tolist(), "pool": res.pool, "per_depth": res.per_depth,
+           "evaluations": res.evaluations, "cost_evaluations": res.cost_evaluations, "search_s": res.seconds,
+           "sweep_calls": quality.sweeps, "best": cfg,
+           "baseline": {"accept": res.baseline.A, "metric": res.baseline.M, "cost_ms": res.baseline.C},
+           "pareto": [{"skip": list(e.skip), "accept": e.A, "metric": e.M, "cost_ms": e.C} for e in res.pareto],
+           "sweep_64_masks_ms": packed * 1e3, "single_verifies_64_masks_ms": single * 1e3,
+           "sweep_speedup": single / packed, "masks_per_s_sweep": 64 / packed, "masks_per_s_single": 64 / single}
+    log(f"search: best {cfg}, {res.evaluations} evaluations in {res.seconds:.1f}s; 64-mask sweep "
+        f"{packed * 1e3:.1f} ms vs {single * 1e3:.1f} ms one verify per mask ({single / packed:.2f}x)")
+    out["latency_us_median"] = packed / 64 * 1e6
+    out["accepted_tok_s"] = None
+    _free(v)
+    return out
+
+
+def workload_domains_13b(args):
+    """13B, 16 requests in two domains whose configurations skip 8 different
+    layers each (from 20-39), admitted through the domain controller (mask
+    set before prefill, 1024-token contexts), one chain k=5 verify per request
+    per round, at most 8 sequences per step.  One round in arrival order
+    (domains interleaved, so each step launches the union of both domains'
+    layers) against one round planned by the controller (a step per domain)."""
+    from paper_2609_26100_amd.controller import ConfigMap, SkipController, plan_cost
+    shape = synth.LLAMA_13B
+    B, n_req, ctx_n, k = 8, 16, 1024, 5
+    layers = np.random.default_rng(13).permutation(np.arange(20, 40))
+    phi = ConfigMap(shape.n_layers, {"translation": {"skip": layers[:8].tolist()},
+                                     "qa": {"skip": layers[8:16].tolist()}})
+    v = _load_verifier(shape, n_seqs=n_req, max_tokens=ctx_n + 16, max_nodes=k + 1, max_batch=B)
+    ctl = SkipController(v, phi)
+    drafts = []
+    for s in range(n_req):
+        ctl.admit(s, "translation" if s % 2 == 0 else "qa")
+        toks = synth.context_tokens(shape.vocab, ctx_n + k + 1, stream=1300 + s)
+        v.prefill(s, toks[:ctx_n])
+        drafts.append(toks[ctx_n:])
+    skip_of = {s: phi.skip_set(ctl.domain_of[s]) for s in range(n_req)}
+    plans = {"arrival_order": [list(range(0, 8)), list(range(8, 16))], "controller": ctl.plan(range(n_req), B)}
+    out = {"workload": "13B-shape, 16 requests in 2 domains (8 skipped layers each), chain k=5, 1024-token contexts",
+           "skip": {d: c.skip for d, c in phi.domains.items()}}
+    for name, plan in plans.items():
+        def rnd(_i, plan=plan):
+            for b in plan:
+                v.verify_batch(b, [drafts[s] for s in b])
+            return 0
+        lat, _ = _timed(rnd, 3, max(5, args.aux_steps // 2))
+        by = sum(batch_bytes(shape, [(phi.mask(ctl.domain_of[s]), ctx_n, k + 1) for s in b]) for b in plan)
+        out[name] = {"round_us_median": float(np.median(lat)) * 1e6, "steps": len(plan),
+                     "blocks_launched": plan_cost(plan, skip_of, shape.n_layers), "algorithmic_GB": by / 1e9,
+                     "roofline_frac": by / PEAK_HBM / float(np.median(lat)), "batches": plan}
+        log(f"domains 13B {name}: {out[name]['round_us_median']:.0f} us per round, "
+            f"{out[name]['blocks_launched']} blocks launched")
+    out["speedup"] = out["arrival_order"]["round_us_median"] / out["controller"]["round_us_median"]
+    out["latency_us_median"] = out["controller"]["round_us_median"]
+    out["accepted_tok_s"] = None
     _free(v)
     return out
 
@@ -446,7 +612,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-reps", type=int, default=5)
     ap.add_argument("--aux-steps", type=int, default=50, help="timed steps of the tree / batch workloads")
-    ap.add_argument("--workloads", default="tree7b,batch13b,sweep33b",
+    ap.add_argument("--workloads", default="decode7b,tree7b,batch13b,domains13b,sweep33b,search7b",
                     help="other workloads to time after the headline one (comma list, or none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--skips", default="0,4,8", help="skip counts to time; the first is the headline")
@@ -476,19 +642,30 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args, shape, d0["mean_accept_len"])
     workloads = {}
-    runners = {"tree7b": workload_tree_7b, "batch13b": workload_batch_13b, "sweep33b": workload_sweep_33b}
+    runners = {"tree7b": workload_tree_7b, "batch13b": workload_batch_13b, "sweep33b": workload_sweep_33b,
+               "decode7b": workload_decode_7b, "search7b": workload_search_7b, "domains13b": workload_domains_13b}
     names = [w for w in args.workloads.split(",") if w and w != "none"]
     for name in names:
         if name not in runners:
             raise SystemExit(f"unknown workload {name}; choose from {sorted(runners)}")
+    # the 7B verifier of the headline serves decode7b and tree7b (which frees it)
+    names = sorted(names, key=lambda w: {"decode7b": 0, "tree7b": 1}.get(w, 2))
     if "tree7b" not in names:
+        if "decode7b" in names:
+            log("workload decode7b")
+            workloads["decode7b"] = workload_decode_7b(args, v7)
+            names.remove("decode7b")
         _free(v7)
     for name in names:
         log(f"workload {name}")
-        workloads[name] = workload_tree_7b(args, v7) if name == "tree7b" else runners[name](args)
+        if name in ("tree7b", "decode7b"):
+            workloads[name] = runners[name](args, v7)
+        else:
+            workloads[name] = runners[name](args)
         w = workloads[name]
-        log(f"workload {name}: median {w['latency_us_median']:.0f} us, "
-            f"{w['accepted_tok_s']:.0f} accepted tok/s")
+        tok_s = w.get("accepted_tok_s")
+        log(f"workload {name}: median {w['latency_us_median']:.0f} us"
+            + (f", {tok_s:.0f} accepted tok/s" if tok_s is not None else ""))
     out = {
         "metric": METRIC,
         "value": d0["accepted_tok_s"],

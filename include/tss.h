@@ -225,6 +225,14 @@ int tss_verify_sweep(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, con
 int tss_get_logits(tss_ctx* ctx, float* host_dst, int32_t n_nodes);
 int tss_get_greedy(tss_ctx* ctx, int32_t* host_dst, int32_t n_nodes);
 
+/* Accepted path of result i of the last verify (i = the sequence's index in
+ * the batch, 0 for tss_verify; for tss_verify_sweep, the mask's index in the
+ * last step): path_nodes[0 .. *path_len) = local node ids from the root to
+ * the deepest accepted node, *path_len = accept_len + 1.  With TSS_COMMIT
+ * these nodes' tokens (after the root) are the committed draft tokens.
+ * path_nodes must hold max_nodes entries. */
+int tss_get_path(tss_ctx* ctx, int32_t index, int32_t* path_nodes, int32_t* path_len);
+
 /* Committed length of a sequence, and rewinding it (n_kv <= current length). */
 int tss_seq_length(tss_ctx* ctx, int32_t seq, int32_t* n_kv);
 int tss_seq_truncate(tss_ctx* ctx, int32_t seq, int32_t n_kv);

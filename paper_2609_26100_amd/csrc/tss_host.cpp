@@ -191,6 +191,7 @@ struct tss_ctx {
   Result* res_host = nullptr;     // [kMaxSegs] host-mapped, written by the accept kernel
   Result* res_dev_map = nullptr;  // its device address
   int last_M = 0;
+  int last_results = 0;  // results (segments) of the last verify step in res_host
   bool poisoned = false;
   std::string err;
   // verify steps replayed from captured HIP graphs, keyed by the step's shape
@@ -1113,6 +1114,7 @@ int verify_batch(tss_ctx* c, int32_t n_seqs, const int32_t* seq_ids, const int32
   const int r = graph ? run_verify_graph(c) : run_step(c, true);
   if (r) return r;
   c->last_M = M;
+  c->last_results = n_seqs;
   for (int i = 0; i < n_seqs; ++i) {
     const int sq = seq_ids[i];
     accept_len[i] = c->res_host[i].accept_len;
@@ -1184,6 +1186,7 @@ int verify_sweep(tss_ctx* c, int32_t seq, const int32_t* tokens, const int32_t* 
     r = run_step(c, true);
     if (r) return r;
     c->last_M = P * n;
+    c->last_results = P;
     for (int i = 0; i < P; ++i) {
       accept_len[k0 + i] = c->res_host[i].accept_len;
       next_token[k0 + i] = c->res_host[i].next_token;
@@ -1273,6 +1276,16 @@ int tss_get_logits(tss_ctx* c, float* host_dst, int32_t n_nodes) {
   HIPCHK(hipStreamSynchronize(c->stream), "sync");
   HIPCHK(hipMemcpy(host_dst, c->ws + c->wsl.logits, (size_t)n_nodes * c->cfg.vocab * 4, hipMemcpyDeviceToHost),
          "logits copy");
+  return TSS_OK;
+}
+
+int tss_get_path(tss_ctx* c, int32_t index, int32_t* path_nodes, int32_t* path_len) {
+  if (!c || !path_nodes || !path_len) return TSS_EINVAL;
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  if (index < 0 || index >= c->last_results) return fail(c, TSS_EINVAL, "no such result in the last verify");
+  const Result& r = c->res_host[index];
+  *path_len = r.path_len;
+  for (int i = 0; i < r.path_len; ++i) path_nodes[i] = r.path[i];
   return TSS_OK;
 }
 

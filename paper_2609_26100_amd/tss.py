@@ -26,7 +26,7 @@ TSS_LAUNCH_DIRECT, TSS_LAUNCH_GRAPH = 0, 1
 EXPORTS = (
     "tss_cfg_check", "tss_weights_bytes", "tss_workspace_bytes", "tss_kv_bytes", "tss_create",
     "tss_load_weights", "tss_kv_alloc", "tss_set_skip_mask", "tss_prefill", "tss_verify", "tss_get_logits",
-    "tss_verify_batch", "tss_verify_sweep", "tss_get_greedy", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
+    "tss_verify_batch", "tss_verify_sweep", "tss_get_greedy", "tss_get_path", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
     "tss_tree_meta", "tss_set_launch_mode", "tss_profile_kernel", "tss_profile_read", "tss_last_error", "tss_status_string",
     "tss_destroy",
 )
@@ -74,6 +74,7 @@ def lib():
             "tss_verify_sweep": (ctypes.c_int, [P, I32, P, P, I32, I32, P, P, P, P]),
             "tss_get_logits": (ctypes.c_int, [P, P, I32]),
             "tss_get_greedy": (ctypes.c_int, [P, P, I32]),
+            "tss_get_path": (ctypes.c_int, [P, I32, P, ctypes.POINTER(I32)]),
             "tss_seq_length": (ctypes.c_int, [P, I32, ctypes.POINTER(I32)]),
             "tss_seq_truncate": (ctypes.c_int, [P, I32, I32]),
             "tss_validate_tree": (ctypes.c_int, [P, I32, I32]),
@@ -219,6 +220,14 @@ def tss_get_greedy(ctx, n_nodes):
     out = np.empty(n_nodes, dtype=np.int32)
     _check(lib().tss_get_greedy(ctx, _ptr(out), n_nodes), ctx, "tss_get_greedy")
     return out
+
+
+def tss_get_path(ctx, index=0, max_nodes=64):
+    """Local node ids of result `index`'s accepted path (root first)."""
+    out = np.zeros(max_nodes, dtype=np.int32)
+    n = ctypes.c_int32()
+    _check(lib().tss_get_path(ctx, index, _ptr(out), ctypes.byref(n)), ctx, "tss_get_path")
+    return out[: n.value].copy()
 
 
 def tss_seq_length(ctx, seq) -> int:

@@ -87,6 +87,10 @@ class Verifier:
     def greedy(self, n_nodes):
         return abi.tss_get_greedy(self.ctx, n_nodes)
 
+    def path(self, index=0):
+        """Accepted path (local node ids, root first) of result `index` of the last verify."""
+        return abi.tss_get_path(self.ctx, index, self.cfg.max_nodes)
+
     def length(self, seq):
         return abi.tss_seq_length(self.ctx, seq)
 

@@ -24,10 +24,11 @@ from .gen import (
     mask_from_layers,
     abi_tensor_loader,
 )
+from .drafter import ReferenceDrafter
 
 __all__ = [
     "ModelShape", "TINY", "LLAMA_7B", "LLAMA_13B", "LLAMA_33B", "SHAPES", "tensor_names", "n_tensors",
     "BASE_SEED", "bf16_round", "bf16_bits", "weight_tensor", "context_tokens", "chain_draft",
     "random_tree", "topk_tree_parents", "tree_draft_tokens", "nested_skip_masks",
-    "random_skip_mask", "mask_from_layers", "abi_tensor_loader",
+    "random_skip_mask", "mask_from_layers", "abi_tensor_loader", "ReferenceDrafter",
 ]

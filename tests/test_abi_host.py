@@ -131,6 +131,7 @@ def test_null_context_calls_fail_cleanly():
     assert L.tss_prefill(None, 0, None, 0) == abi.TSS_EINVAL
     assert L.tss_verify_batch(None, 1, None, None, None, None, None, 0, None, None) == abi.TSS_EINVAL
     assert L.tss_verify_sweep(None, 0, None, None, 1, 1, None, None, None, None) == abi.TSS_EINVAL
+    assert L.tss_get_path(None, 0, None, None) == abi.TSS_EINVAL
     assert L.tss_set_skip_mask(None, 0, None) == abi.TSS_EINVAL
     assert L.tss_load_weights(None, 0, 1, None) == abi.TSS_EINVAL
     L.tss_destroy(None)
