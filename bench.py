@@ -227,6 +227,7 @@ def _free(v):
     import torch
     v.close()
     del v.weights, v.workspace, v.kv_pool
+    v.prefix = None
     torch.cuda.empty_cache()
 
 

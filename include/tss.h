@@ -207,17 +207,32 @@ int tss_verify_batch(tss_ctx* ctx, int32_t n_seqs, const int32_t* seq_ids, const
  *     otherwise; prefill the sequence dense for a sweep).
  *   accept_len[n_masks], next_token[n_masks]: mask k's decision.
  *   greedy: n_masks * n_nodes greedy tokens (mask k's at k * n_nodes), or NULL.
- * Consecutive masks are verified together as segments of one step (at most
- * 32, at most min(max_nodes * max_batch, 128) rows, and only as many as the
- * sequence's free KV slots hold: each segment writes its draft K/V to its own
- * slots after the context).  Such a step launches each block that any of its
- * masks runs once, reading its weights and each context page once for all
- * of them, so callers should order masks that share skipped layers next to
- * each other.  The sequence's length and committed K/V are unchanged;
- * tss_get_logits / tss_get_greedy then return the last step's rows. */
+ *   dev_prefix, prefix_bytes: NULL / 0, or a device buffer of at least
+ *     tss_sweep_prefix_bytes(cfg, n_nodes) bytes (TSS_ENOSPACE otherwise)
+ *     that the call may overwrite: with it the masks are ordered by their
+ *     first skipped layer and, when that saves more blocks than it costs, one
+ *     dense pass stores every node's residual before every layer; each step
+ *     then starts at the earliest first-skipped layer of its masks from the
+ *     stored residual (a mask runs every layer before its first skipped one
+ *     exactly as the dense verifier does), and the dense pass answers the
+ *     masks that skip nothing.
+ * Masks are verified together as segments of one step (at most 32, at most
+ * min(max_nodes * max_batch, 128) rows, and only as many as the sequence's
+ * free KV slots hold: each segment writes its draft K/V to its own slots
+ * after the context).  Such a step launches each block that any of its masks
+ * runs once, reading its weights and each context page once for all of
+ * them; without a prefix buffer consecutive masks share steps, so callers
+ * should order masks that share skipped layers next to each other.  The
+ * sequence's length and committed K/V are unchanged; tss_get_logits /
+ * tss_get_greedy / tss_get_path then describe the last step's segments. */
 int tss_verify_sweep(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent,
                      int32_t n_nodes, int32_t n_masks, const uint8_t* skip_masks, int32_t* accept_len,
-                     int32_t* next_token, int32_t* greedy);
+                     int32_t* next_token, int32_t* greedy, void* dev_prefix, size_t prefix_bytes);
+
+/* Bytes of the prefix buffer of tss_verify_sweep for trees of n_nodes nodes:
+ * n_layers * n_nodes * d_model fp32 values (0 when cfg or n_nodes is
+ * invalid). */
+size_t tss_sweep_prefix_bytes(const tss_model_cfg* cfg, int32_t n_nodes);
 
 /* Copies the last verify's fp32 logits [n_nodes][vocab] / greedy tokens
  * [n_nodes] to host memory (rows in the step's node order).  n_nodes must not

@@ -5,7 +5,7 @@
 
 namespace tss {
 
-// h[m] = E[tok[m]] (fp32); xn[m] = h[m] * gain (activation planes) with the
+// h[m] = E[tok[m]] (fp32), or a saved residual row (src_h); xn[m] = h[m] * gain (activation planes) with the
 // gain of the first RMSNorm the row's sequence meets; ss_out[m][p] = sum of
 // h[m][k]^2 over the 16 columns of part p (the format every projection
 // epilogue writes, so each norm reads d/16 parts whatever produced them).
@@ -26,6 +26,29 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     for (int i = threadIdx.x; i < (int)(sizeof(StepParams) / 4); i += 256) dst[i] = src[i];
   }
   const float* gain = a.gain[a.sp.row_seq[m]];
+  if (a.src_h) {
+    // resume from a saved residual row (fp32, 16 bytes per chunk)
+    const float4* src = (const float4*)(a.src_h + (size_t)(m - a.sp.seq_row0[a.sp.row_seq[m]]) * d);
+    for (int c = threadIdx.x; c < d / 4; c += 256) {
+      const float4 v4 = src[c];
+      const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int k = c * 4 + j;
+        a.h[(size_t)m * d + k] = vv[j];
+        store_act<T>(a.xn, a.xn_plane, act_index<T>(m, k, d), vv[j] * gain[k]);
+        rowv[k] = vv[j];
+      }
+    }
+    __syncthreads();
+    for (int p = threadIdx.x; p < d / 16; p += 256) {
+      float s = 0.f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) s += rowv[p * 16 + k] * rowv[p * 16 + k];
+      a.ss_out[(size_t)m * a.ss_stride + p] = s;
+    }
+    return;
+  }
   const T* row = (const T*)a.embed + (size_t)a.sp.tok[m] * d;
   uint4 raw[MAXC];
 #pragma unroll

@@ -644,7 +644,7 @@ struct ProfScope {
   }
 };
 
-EmbedArgs embed_args(tss_ctx* c);
+EmbedArgs embed_args(tss_ctx* c, int start_layer = 0, const float* src_h = nullptr);
 
 
 // Layer after `l` that segment i runs (n_layers = none), and the gain of the
@@ -670,7 +670,14 @@ const float* attn_gain_of(const tss_ctx* c, int layer) {
 // sequences, masks, node counts, compaction), not on context lengths, so a
 // captured sequence of launches can be replayed for later steps of the same
 // shape.
-int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
+//
+// start_layer > 0 resumes a step after blocks that every segment runs as the
+// dense verifier does: the rows start from resume_h (the residual before
+// start_layer of each local node, [n][d] fp32) instead of the embedding.
+// save_prefix, when set, receives the residual of rows 0 .. prefix_rows-1
+// before every block l >= 1 (at save_prefix + l * prefix_rows * d).
+int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, const float* resume_h = nullptr,
+                 float* save_prefix = nullptr, int prefix_rows = 0) {
   const tss_model_cfg& cf = c->cfg;
   const StepParams& sp = *c->sp_host;
   const tss_ctx::Step& st = c->step;
@@ -698,7 +705,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
   for (int i = 0; i < n_arg_pages; ++i) arg_pages[i] = c->pt_host[(size_t)pt_off[0] + i];
 
   {
-    const EmbedArgs a = embed_args(c);
+    const EmbedArgs a = embed_args(c, start_layer, start_layer > 0 ? resume_h : nullptr);
     ProfScope ps(c, TSS_K_EMBED, -1);
     HIPCHK(launch_embed(c->bf16, a, s), "embed");
     ps.done();
@@ -718,7 +725,11 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s) {
   base.sp = sp_dev;
   base.row_on[0] = base.row_on[1] = ~0ull;
 
-  for (int l = 0; l < L; ++l) {
+  for (int l = start_layer; l < L; ++l) {
+    if (save_prefix && l > 0)
+      HIPCHK(hipMemcpyAsync(save_prefix + (size_t)l * prefix_rows * d, ws + c->wsl.h, (size_t)prefix_rows * d * 4,
+                            hipMemcpyDeviceToDevice, s),
+             "prefix save");
     // rows and segments that run block l; attention items: per KV sequence
     // (a run of segments with the same sequence), the rows from its first to
     // its last segment that runs the block, cut into pieces of 64 rows
@@ -926,22 +937,26 @@ int finish_step(tss_ctx* c) {
   return TSS_OK;
 }
 
-int run_step(tss_ctx* c, bool verify) {
-  const int r = enqueue_step(c, verify, c->stream);
+int run_step(tss_ctx* c, bool verify, int start_layer = 0, const float* resume_h = nullptr,
+             float* save_prefix = nullptr, int prefix_rows = 0) {
+  const int r = enqueue_step(c, verify, c->stream, start_layer, resume_h, save_prefix, prefix_rows);
   if (r) return r;
   return finish_step(c);
 }
 
 // The embedding kernel's arguments for the step in c->sp_host (the only
-// per-step arguments of a verify).
-EmbedArgs embed_args(tss_ctx* c) {
+// per-step arguments of a verify); a resumed step starts at start_layer from
+// the saved residual rows src_h.
+EmbedArgs embed_args(tss_ctx* c, int start_layer, const float* src_h) {
   const tss_model_cfg& cf = c->cfg;
   const StepParams& sp = *c->sp_host;
   EmbedArgs a{};
   a.embed = c->w + c->wl.embed;
   a.sp = sp;
   a.sp_dev = (StepParams*)(c->ws + c->wsl.sp);
-  for (int i = 0; i < kMaxSegs; ++i) a.gain[i] = attn_gain_of(c, i < c->step.n_seqs ? next_active(c, i, -1) : 0);
+  for (int i = 0; i < kMaxSegs; ++i)
+    a.gain[i] = attn_gain_of(c, i < c->step.n_seqs ? next_active(c, i, start_layer - 1) : 0);
+  a.src_h = src_h;
   a.h = (float*)(c->ws + c->wsl.h);
   a.xn = c->ws + c->wsl.xa;
   a.xn_plane = act_planes(&cf) == 2 ? (size_t)c->Mp * cf.d_model : 0;
@@ -1136,8 +1151,21 @@ int verify_batch(tss_ctx* c, int32_t n_seqs, const int32_t* seq_ids, const int32
 // all of its masks.  Direct launches: sweep steps rarely repeat a shape, and
 // capturing each would cost more than it saves and evict the decode steps'
 // graphs.
+//
+// With a prefix buffer, the shared prefix is reused as well: a mask runs
+// every block before its first skipped one exactly as the dense verifier
+// does, so the masks are ordered by their first skipped block (latest first),
+// one dense pass saves every node's residual before every block, and each
+// step starts at the earliest first-skipped block among its masks from that
+// saved residual.  The dense pass itself answers the dense masks.  It is
+// taken only when the blocks it saves exceed the blocks it costs.
+size_t sweep_prefix_bytes(const tss_model_cfg* cf, int n) {
+  return (size_t)cf->n_layers * n * cf->d_model * 4;
+}
+
 int verify_sweep(tss_ctx* c, int32_t seq, const int32_t* tokens, const int32_t* parent, int32_t n,
-                 int32_t n_masks, const uint8_t* masks, int32_t* accept_len, int32_t* next_token, int32_t* greedy) {
+                 int32_t n_masks, const uint8_t* masks, int32_t* accept_len, int32_t* next_token, int32_t* greedy,
+                 void* prefix, size_t prefix_bytes) {
   int r = check_ready(c, seq);
   if (r) return r;
   if (!tokens || !masks || !accept_len || !next_token) return fail(c, TSS_EINVAL, "null argument");
@@ -1148,6 +1176,8 @@ int verify_sweep(tss_ctx* c, int32_t seq, const int32_t* tokens, const int32_t* 
     if (tokens[j] < 0 || tokens[j] >= c->cfg.vocab) return fail(c, TSS_EINVAL, "token outside [0, vocab)");
   const int L = c->cfg.n_layers;
   if (!mask_ok(masks, n_masks * L)) return fail(c, TSS_EINVAL, "mask bytes must be 0 or 1");
+  if (prefix && prefix_bytes < sweep_prefix_bytes(&c->cfg, n))
+    return fail(c, TSS_ENOSPACE, "prefix buffer smaller than tss_sweep_prefix_bytes");
   if (c->n_kv[seq] + n > c->max_tokens) return fail(c, TSS_ECAPACITY, "verify exceeds the sequence's KV capacity");
   for (int k = 0; k < n_masks; ++k)
     for (int l = 0; l < L; ++l)
@@ -1158,15 +1188,36 @@ int verify_sweep(tss_ctx* c, int32_t seq, const int32_t* tokens, const int32_t* 
   int32_t depth[kMaxNodes];
   uint64_t anc[kMaxNodes];
   tree_meta(parent, n, depth, anc);
+
+  // first skipped block of each mask (L: dense), and the order of the masks
+  std::vector<int> first(n_masks, L), ord(n_masks);
+  for (int k = 0; k < n_masks; ++k) {
+    ord[k] = k;
+    for (int l = 0; l < L; ++l)
+      if (masks[(size_t)k * L + l]) {
+        first[k] = l;
+        break;
+      }
+  }
+  int n_dense = 0;
+  bool reuse = false;
+  if (prefix) {
+    std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) { return first[x] > first[y]; });
+    while (n_dense < n_masks && first[ord[n_dense]] == L) ++n_dense;
+    long saved = 0;
+    for (int k0 = n_dense; k0 < n_masks; k0 += per_step) saved += first[ord[std::min(k0 + per_step, n_masks) - 1]];
+    reuse = saved > L;
+  }
+  float* pre = (float*)prefix;
+  const int d = c->cfg.d_model;
+
   tss_ctx::Step& st = c->step;
-  for (int k0 = 0; k0 < n_masks; k0 += per_step) {
-    const int P = std::min(per_step, n_masks - k0);
+  auto fill = [&](int P) {  // the step's parameters for P segments of the tree
     StepParams& sp = *c->sp_host;
     std::memset(&sp, 0, sizeof(sp));
     sp.M = P * n;
     sp.n_seqs = P;
     st.n_seqs = P;
-    st.mask.assign(masks + (size_t)k0 * L, masks + (size_t)(k0 + P) * L);
     for (int i = 0; i < P; ++i) {
       const int r0 = i * n;
       st.seq[i] = seq;
@@ -1183,17 +1234,45 @@ int verify_sweep(tss_ctx* c, int32_t seq, const int32_t* tokens, const int32_t* 
       }
     }
     sp.seq_row0[P] = P * n;
-    r = run_step(c, true);
-    if (r) return r;
+  };
+  auto collect = [&](const int* ks, int P) -> int {  // results of mask ks[i] from segment i
     c->last_M = P * n;
     c->last_results = P;
     for (int i = 0; i < P; ++i) {
-      accept_len[k0 + i] = c->res_host[i].accept_len;
-      next_token[k0 + i] = c->res_host[i].next_token;
+      accept_len[ks[i]] = c->res_host[i].accept_len;
+      next_token[ks[i]] = c->res_host[i].next_token;
     }
-    if (greedy)
-      HIPCHK(hipMemcpy(greedy + (size_t)k0 * n, c->ws + c->wsl.greedy, (size_t)P * n * 4, hipMemcpyDeviceToHost),
-             "greedy copy");
+    if (greedy) {
+      std::vector<int32_t> g((size_t)P * n);
+      HIPCHK(hipMemcpy(g.data(), c->ws + c->wsl.greedy, (size_t)P * n * 4, hipMemcpyDeviceToHost), "greedy copy");
+      for (int i = 0; i < P; ++i) std::memcpy(greedy + (size_t)ks[i] * n, g.data() + (size_t)i * n, (size_t)n * 4);
+    }
+    return TSS_OK;
+  };
+
+  int k0 = 0;
+  if (reuse) {
+    // the dense pass: saves the prefix, answers the dense masks
+    fill(1);
+    st.mask.assign(L, 0);
+    r = run_step(c, true, 0, nullptr, pre, n);
+    if (r) return r;
+    for (int k = 0; k < n_dense; ++k) {
+      r = collect(&ord[k], 1);
+      if (r) return r;
+    }
+    k0 = n_dense;
+  }
+  for (; k0 < n_masks; k0 += per_step) {
+    const int P = std::min(per_step, n_masks - k0);
+    fill(P);
+    st.mask.resize((size_t)P * L);
+    for (int i = 0; i < P; ++i) std::memcpy(st.mask.data() + (size_t)i * L, masks + (size_t)ord[k0 + i] * L, L);
+    const int start = reuse ? first[ord[k0 + P - 1]] : 0;  // the earliest first skip of the step
+    r = run_step(c, true, start, start > 0 ? pre + (size_t)start * n * d : nullptr);
+    if (r) return r;
+    r = collect(&ord[k0], P);
+    if (r) return r;
   }
   return TSS_OK;
 }
@@ -1202,12 +1281,16 @@ int verify_sweep(tss_ctx* c, int32_t seq, const int32_t* tokens, const int32_t* 
 
 extern "C" {
 
+size_t tss_sweep_prefix_bytes(const tss_model_cfg* cfg, int32_t n_nodes) {
+  return cfg_ok(cfg) && n_nodes >= 1 && n_nodes <= cfg->max_nodes ? sweep_prefix_bytes(cfg, n_nodes) : 0;
+}
+
 int tss_verify_sweep(tss_ctx* c, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent,
                      int32_t n_nodes, int32_t n_masks, const uint8_t* skip_masks, int32_t* accept_len,
-                     int32_t* next_token, int32_t* greedy) {
+                     int32_t* next_token, int32_t* greedy, void* dev_prefix, size_t prefix_bytes) {
   if (!c) return TSS_EINVAL;
   return verify_sweep(c, seq, draft_tokens, tree_parent, n_nodes, n_masks, skip_masks, accept_len, next_token,
-                      greedy);
+                      greedy, dev_prefix, prefix_bytes);
 }
 
 int tss_prefill(tss_ctx* c, int32_t seq, const int32_t* tokens, int32_t n) {

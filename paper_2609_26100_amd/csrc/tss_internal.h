@@ -203,6 +203,10 @@ struct AttnArgs {
 
 struct EmbedArgs {
   const void* embed;       // [V][d] T
+  // when set, row m starts from a saved residual instead of its token's
+  // embedding: src_h[j][d] fp32 with j = m's local node (a step that resumes
+  // after blocks every segment shares with the dense verifier)
+  const float* src_h;
   StepParams sp;           // this step's parameters (by value) ...
   StepParams* sp_dev;      // ... copied here for the later kernels of the step
   const float* gain[kMaxSegs];   // per segment: gain of the first RMSNorm its rows meet

@@ -26,7 +26,7 @@ TSS_LAUNCH_DIRECT, TSS_LAUNCH_GRAPH = 0, 1
 EXPORTS = (
     "tss_cfg_check", "tss_weights_bytes", "tss_workspace_bytes", "tss_kv_bytes", "tss_create",
     "tss_load_weights", "tss_kv_alloc", "tss_set_skip_mask", "tss_prefill", "tss_verify", "tss_get_logits",
-    "tss_verify_batch", "tss_verify_sweep", "tss_get_greedy", "tss_get_path", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
+    "tss_verify_batch", "tss_verify_sweep", "tss_sweep_prefix_bytes", "tss_get_greedy", "tss_get_path", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
     "tss_tree_meta", "tss_set_launch_mode", "tss_profile_kernel", "tss_profile_read", "tss_last_error", "tss_status_string",
     "tss_destroy",
 )
@@ -71,7 +71,8 @@ def lib():
             "tss_prefill": (ctypes.c_int, [P, I32, P, I32]),
             "tss_verify": (ctypes.c_int, [P, I32, P, P, I32, P, U32, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
             "tss_verify_batch": (ctypes.c_int, [P, I32, P, P, P, P, P, U32, P, P]),
-            "tss_verify_sweep": (ctypes.c_int, [P, I32, P, P, I32, I32, P, P, P, P]),
+            "tss_verify_sweep": (ctypes.c_int, [P, I32, P, P, I32, I32, P, P, P, P, P, SZ]),
+            "tss_sweep_prefix_bytes": (SZ, [CFG, I32]),
             "tss_get_logits": (ctypes.c_int, [P, P, I32]),
             "tss_get_greedy": (ctypes.c_int, [P, P, I32]),
             "tss_get_path": (ctypes.c_int, [P, I32, P, ctypes.POINTER(I32)]),
@@ -192,10 +193,16 @@ def tss_verify_batch(ctx, seq_ids, draft_tokens, node_offsets, tree_parents=None
     return al, nt
 
 
-def tss_verify_sweep(ctx, seq, draft_tokens, tree_parent, skip_masks, want_greedy=False):
+def tss_sweep_prefix_bytes(cfg, n_nodes) -> int:
+    return lib().tss_sweep_prefix_bytes(ctypes.byref(cfg), n_nodes)
+
+
+def tss_verify_sweep(ctx, seq, draft_tokens, tree_parent, skip_masks, want_greedy=False, dev_prefix=None,
+                     prefix_bytes=0):
     """Dry-run verifies of one draft tree under each row of skip_masks
     [n_masks][n_layers]; returns (accept_len[n_masks], next_token[n_masks]) and,
-    with want_greedy, greedy[n_masks][n_nodes]."""
+    with want_greedy, greedy[n_masks][n_nodes].  dev_prefix: device pointer of
+    a prefix buffer (tss_sweep_prefix_bytes) or None."""
     t = np.ascontiguousarray(draft_tokens, dtype=np.int32)
     p = None if tree_parent is None else np.ascontiguousarray(tree_parent, dtype=np.int32)
     m = np.ascontiguousarray(skip_masks, dtype=np.uint8)
@@ -205,8 +212,8 @@ def tss_verify_sweep(ctx, seq, draft_tokens, tree_parent, skip_masks, want_greed
     al = np.zeros(k, dtype=np.int32)
     nt = np.zeros(k, dtype=np.int32)
     g = np.zeros((k, len(t)), dtype=np.int32) if want_greedy else None
-    _check(lib().tss_verify_sweep(ctx, seq, _ptr(t), _ptr(p), len(t), k, _ptr(m), _ptr(al), _ptr(nt), _ptr(g)),
-           ctx, "tss_verify_sweep")
+    _check(lib().tss_verify_sweep(ctx, seq, _ptr(t), _ptr(p), len(t), k, _ptr(m), _ptr(al), _ptr(nt), _ptr(g),
+                                  dev_prefix, prefix_bytes), ctx, "tss_verify_sweep")
     return (al, nt, g) if want_greedy else (al, nt)
 
 

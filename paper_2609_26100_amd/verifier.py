@@ -34,6 +34,7 @@ class Verifier:
         abi.tss_kv_alloc(self.ctx, n_seqs, max_tokens, self.kv_pool.data_ptr(), kb, page_order)
         self.n_seqs, self.max_tokens = n_seqs, max_tokens
         self._mask = {i: np.zeros(shape.n_layers, np.uint8) for i in range(n_seqs)}
+        self.prefix = None  # device buffer of the mask sweep's shared prefix
 
     def load(self, get_tensor):
         """Streams every tensor, in the ABI's tensor order, from get_tensor(index) -> host array in the
@@ -75,11 +76,19 @@ class Verifier:
             assert m.size == L * len(seqs)
         return abi.tss_verify_batch(self.ctx, seqs, tokens, offs, par, m, abi.TSS_COMMIT if commit else 0)
 
-    def verify_sweep(self, seq, tokens, masks, parent=None, want_greedy=False):
+    def verify_sweep(self, seq, tokens, masks, parent=None, want_greedy=False, reuse_prefix=True):
         """Dry runs of one draft tree under each mask (rows of masks); returns
-        (accept_len[k], next_token[k]) and, with want_greedy, greedy[k][n]."""
+        (accept_len[k], next_token[k]) and, with want_greedy, greedy[k][n].
+        With reuse_prefix the masks share the dense prefix through a device
+        buffer owned by this verifier (allocated on first use)."""
         m = np.asarray(masks, dtype=np.uint8).reshape(-1, self.shape.n_layers)
-        return abi.tss_verify_sweep(self.ctx, seq, tokens, parent, m, want_greedy)
+        ptr, nbytes = None, 0
+        if reuse_prefix:
+            nbytes = abi.tss_sweep_prefix_bytes(self.cfg, self.cfg.max_nodes)
+            if self.prefix is None:
+                self.prefix = self.torch.empty(nbytes, dtype=self.torch.uint8, device=self.device)
+            ptr = self.prefix.data_ptr()
+        return abi.tss_verify_sweep(self.ctx, seq, tokens, parent, m, want_greedy, ptr, nbytes)
 
     def logits(self, n_nodes):
         return abi.tss_get_logits(self.ctx, n_nodes, self.shape.vocab)

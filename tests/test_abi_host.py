@@ -130,7 +130,7 @@ def test_null_context_calls_fail_cleanly():
     assert L.tss_verify(None, 0, None, None, 1, None, 0, ctypes.byref(al), ctypes.byref(nt)) == abi.TSS_EINVAL
     assert L.tss_prefill(None, 0, None, 0) == abi.TSS_EINVAL
     assert L.tss_verify_batch(None, 1, None, None, None, None, None, 0, None, None) == abi.TSS_EINVAL
-    assert L.tss_verify_sweep(None, 0, None, None, 1, 1, None, None, None, None) == abi.TSS_EINVAL
+    assert L.tss_verify_sweep(None, 0, None, None, 1, 1, None, None, None, None, None, 0) == abi.TSS_EINVAL
     assert L.tss_get_path(None, 0, None, None) == abi.TSS_EINVAL
     assert L.tss_set_skip_mask(None, 0, None) == abi.TSS_EINVAL
     assert L.tss_load_weights(None, 0, 1, None) == abi.TSS_EINVAL
@@ -140,3 +140,10 @@ def test_null_context_calls_fail_cleanly():
 def test_status_strings():
     for s in (abi.TSS_OK, abi.TSS_EINVAL, abi.TSS_ENOSPACE, abi.TSS_ECAPACITY, abi.TSS_ESTATE, abi.TSS_EHIP):
         assert abi.tss_status_string(s) not in ("", "unknown status")
+
+
+def test_sweep_prefix_bytes():
+    cfg = abi.make_cfg(synth.LLAMA_7B, 64)
+    assert abi.tss_sweep_prefix_bytes(cfg, 33) == 32 * 33 * 4096 * 4
+    assert abi.tss_sweep_prefix_bytes(cfg, 0) == 0
+    assert abi.tss_sweep_prefix_bytes(cfg, 65) == 0

@@ -32,8 +32,8 @@ def _compare_sweep(shape, v, m, o, tokens, parent, masks, per_step):
     decisions compared."""
     tol, gate = TOL[shape.dtype]
     n = len(tokens)
-    al, nt, g = v.verify_sweep(0, tokens, masks, parent, want_greedy=True)
-    last = len(masks) - (len(masks) - 1) % per_step - 1  # first mask of the last step
+    al, nt, g = v.verify_sweep(0, tokens, masks, parent, want_greedy=True, reuse_prefix=False)
+    last = len(masks) - (len(masks) - 1) % per_step - 1  # first mask of the last step (caller order)
     lg = v.logits((len(masks) - last) * n)
     compared = rows = 0
     for k, mk in enumerate(masks):
@@ -175,4 +175,76 @@ def test_13b_dims_sweep_of_16_masks_vs_oracle():
     comp = _compare_sweep(SHAPE13, v, m, o, tokens, parent, masks, per_step=7)
     assert comp >= 4
     assert v.length(0) == 333
+    v.close()
+
+
+def _late_masks(n_layers):
+    """The dense mask and every mask that runs layer 0 (first skip >= 1)."""
+    return np.array([m for m in _all_masks(n_layers) if m[0] == 0], dtype=np.uint8)
+
+
+def _prefix_case(shape, v, m, ctx_n, n, stream, random_gains):
+    o = OracleSequence(m, np.zeros(shape.n_layers, np.uint8))
+    ctx = synth.context_tokens(shape.vocab, ctx_n, stream=stream)
+    v.prefill(0, ctx)
+    prefill(m, o, ctx)
+    tokens = synth.context_tokens(shape.vocab, n, stream=stream + 1)
+    parent = synth.random_tree(n, stream=stream + 2, max_children=3)
+    return o, tokens, parent
+
+
+def _sweep_vs_oracle(shape, v, m, o, tokens, parent, masks, reuse):
+    """Every mask's greedy tokens and decision against the oracle; the last
+    step's logits (one or more masks, the last in first-skip order) too."""
+    tol, gate = TOL[shape.dtype]
+    n = len(tokens)
+    al, nt, g = v.verify_sweep(0, tokens, masks, parent, want_greedy=True, reuse_prefix=reuse)
+    res = [verify(m, o, np.asarray(tokens), parent, mk) for mk in masks]
+    compared = 0
+    for k, r in enumerate(res):
+        sure = r.margin > gate
+        np.testing.assert_array_equal(g[k][sure], r.greedy[sure], err_msg=f"mask {k}")
+        if min(float(r.margin[i]) for i in r.path) > gate:
+            assert (int(al[k]), int(nt[k])) == (r.accept_len, r.next_token), f"mask {k}"
+            compared += 1
+    return al, nt, g, res, compared
+
+
+def test_tiny_sweep_prefix_reuse_one_mask_per_step():
+    """8 free slots for an 8-node tree: one mask per step, so every step after
+    the dense pass resumes at its mask's first skipped layer."""
+    v = gpu_verifier(TINY, random_gains=True, n_seqs=1, max_tokens=88, max_nodes=8, max_batch=8)
+    m = oracle_model(TINY, random_gains=True)
+    o, tokens, parent = _prefix_case(TINY, v, m, 80, 8, 2200, True)
+    masks = _late_masks(TINY.n_layers)          # dense, 0001, 0010, ..., 0111
+    al, nt, g, res, comp = _sweep_vs_oracle(TINY, v, m, o, tokens, parent, masks, reuse=True)
+    # the last step is mask 0100 or later in first-skip order: a step resumed at layer 1
+    last = [k for k in range(len(masks)) if masks[k][1] == 1][-1]
+    err = float(np.max(np.abs(v.logits(8) - res[last].logits)))
+    log(f"tiny prefix reuse: {comp}/{len(masks)} decisions compared, resumed step logits max-abs {err:.2e}")
+    assert err <= TOL["f32"][0]
+    assert comp >= 6
+    al2, nt2, g2 = v.verify_sweep(0, tokens, masks, parent, want_greedy=True, reuse_prefix=False)
+    np.testing.assert_array_equal(al2, al)
+    np.testing.assert_array_equal(nt2, nt)
+    assert (g2 == g).mean() > 0.99
+    assert v.length(0) == 80
+    v.close()
+
+
+def test_13b_dims_sweep_prefix_reuse_vs_oracle():
+    """Two masks per step (rows 34), masks that all run layer 0: after the
+    dense pass, steps {0001, 0010}, {0011, 0100}, {0101, 0110}, {0111}
+    resume at layers 2, 1, 1 and 1 from its saved residual."""
+    log("building the 4-layer 13B-dimension bf16 model (prefix reuse, 17-node tree)")
+    v = gpu_verifier(SHAPE13, n_seqs=1, max_tokens=400, max_nodes=17, max_batch=2)
+    m = oracle_model(SHAPE13)
+    o, tokens, parent = _prefix_case(SHAPE13, v, m, 257, 17, 2300, False)
+    masks = _late_masks(4)
+    al, nt, g, res, comp = _sweep_vs_oracle(SHAPE13, v, m, o, tokens, parent, masks, reuse=True)
+    err = float(np.max(np.abs(v.logits(17) - res[7].logits)))   # the last step: mask 0111 alone
+    log(f"13B dims prefix reuse: {comp}/8 decisions compared, resumed step logits max-abs {err:.2e}")
+    assert err <= TOL["bf16"][0]
+    assert comp >= 3
+    assert v.length(0) == 257
     v.close()
