@@ -334,7 +334,9 @@ def workload_batch_13b(args):
 def workload_sweep_33b(args):
     """33B, one 4096-token context prefilled dense, 32-node tree + root (depth
     5, branching 4,3,2,1,1, quotas 4,10,10,5,3), 64 masks of U{4..16} layers
-    from 2-59 verified back to back as dry runs (timing only)."""
+    from 2-59 verified back to back as dry runs (timing only); then the same
+    64 masks through the packed sweep (3 masks per step), without and with
+    reuse of the shared dense prefix."""
     shape = synth.LLAMA_33B
     ctx_n = 4096
     v = _load_verifier(shape, n_seqs=1, max_tokens=ctx_n + 112, max_nodes=33, max_batch=4)
@@ -369,12 +371,32 @@ def workload_sweep_33b(args):
         acc_all.append(acc)
         by_all.append(by)
     all_masks = np.stack(masks)
-    v.verify_sweep(0, tokens, all_masks, parent)
-    t0 = time.perf_counter()
-    for _ in range(n_steps):
-        v.verify_sweep(0, tokens, all_masks, parent)
-    packed = (time.perf_counter() - t0) / n_steps
-    log(f"33B sweep: 64 masks packed {packed * 1e3:.1f} ms vs {sum(p[1] for p in per_mask) / 1e3:.1f} ms one by one")
+
+    def sweep_ms(reuse):
+        v.verify_sweep(0, tokens, all_masks, parent, reuse_prefix=reuse)
+        t0 = time.perf_counter()
+        for _ in range(n_steps):
+            v.verify_sweep(0, tokens, all_masks, parent, reuse_prefix=reuse)
+        return (time.perf_counter() - t0) / n_steps
+    packed_plain = sweep_ms(False)
+    packed = sweep_ms(True)
+    # the first evaluations of the breadth search: dense and every single-layer skip
+    singles = np.zeros((shape.n_layers + 1, shape.n_layers), np.uint8)
+    for l in range(shape.n_layers):
+        singles[l + 1, l] = 1
+
+    def singles_ms(reuse):
+        v.verify_sweep(0, tokens, singles, parent, reuse_prefix=reuse)
+        t0 = time.perf_counter()
+        for _ in range(n_steps):
+            v.verify_sweep(0, tokens, singles, parent, reuse_prefix=reuse)
+        return (time.perf_counter() - t0) / n_steps
+    singles_plain = singles_ms(False)
+    singles_reuse = singles_ms(True)
+    log(f"33B sweep: dense + 60 single-layer skips packed {singles_plain * 1e3:.1f} ms, "
+        f"with prefix reuse {singles_reuse * 1e3:.1f} ms")
+    log(f"33B sweep: 64 masks packed {packed_plain * 1e3:.1f} ms, with prefix reuse {packed * 1e3:.1f} ms, "
+        f"{sum(p[1] for p in per_mask) / 1e3:.1f} ms one by one")
     sk = np.array([p[0] for p in per_mask], float)
     us = np.array([p[1] for p in per_mask])
     slope, icpt = np.polyfit(sk, us, 1)
@@ -390,7 +412,9 @@ def workload_sweep_33b(args):
            "roofline_us_per_skipped_layer": batch_bytes(shape, [(np.zeros(shape.n_layers), ctx_n, 33)]) / PEAK_HBM * 1e6
            - batch_bytes(shape, [(synth.mask_from_layers(shape.n_layers, [2]), ctx_n, 33)]) / PEAK_HBM * 1e6,
            "per_mask": [{"skipped": p[0], "latency_us": p[1], "roofline_frac": p[2]} for p in per_mask],
-           "packed_sweep_ms": packed * 1e3, "one_by_one_ms": sum(p[1] for p in per_mask) / 1e3,
+           "packed_sweep_ms": packed * 1e3, "packed_sweep_no_prefix_reuse_ms": packed_plain * 1e3,
+           "one_by_one_ms": sum(p[1] for p in per_mask) / 1e3,
+           "singles_61_masks_packed_ms": singles_plain * 1e3, "singles_61_masks_prefix_reuse_ms": singles_reuse * 1e3,
            "packed_speedup": sum(p[1] for p in per_mask) / 1e6 / packed}
     _free(v)
     return out

@@ -130,6 +130,80 @@ def breadth_search(n_layers, max_depth, quality, cost, eps_A, eps_M, tau_A, tau_
                         len(entries), len(costs), entries, costs, time.perf_counter() - t0)
 
 
+def beam_search(n_layers, quality, cost, beam_width=3, early_barrier=2, latter_barrier=0, score_tol=0.05,
+                min_skips=3, max_depth=None, log=None):
+    """The beam-style search of the paper's hyperparameter table (Table 3), an
+    alternative to Algorithm 1's exhaustive depths.  Reading of its settings:
+
+    * candidates: layers [early_barrier, n_layers - latter_barrier), tried
+      latter to early;
+    * depth by depth, every beam entry grows by one candidate layer; a child
+      is kept only if A >= A_dense (hard acceptance constraint) and
+      M >= (1 - score_tol) M_dense (relative score tolerance);
+    * the kept children are ranked by acceptance, then number of skipped
+      layers, then tok/s = A / C (all descending, first met on ties) and the
+      best beam_width form the next beam; the search stops when none is kept;
+    * selection: among every kept configuration, the "triple wins" (metric,
+      acceptance and tok/s all >= the dense verifier's), preferring those with
+      at least min(min_skips, largest |S| kept) skipped layers, ranked as
+      above; the dense verifier when there is none.
+
+    Returns a SearchResult (pool = candidate layers, feasible = kept sets in
+    the order met, pareto = the selection ranking of the triple wins)."""
+    t0 = time.perf_counter()
+    entries, costs = {}, {}
+
+    def q(sets):
+        todo = [S for S in sets if S not in entries]
+        if todo:
+            A, M = quality(todo)
+            for S, a, m in zip(todo, A, M):
+                entries[S] = (float(a), float(m))
+        return [entries[S] for S in sets]
+
+    def c(sets):
+        todo = [S for S in sets if S not in costs]
+        if todo:
+            for S, v in zip(todo, cost(todo)):
+                costs[S] = float(v)
+        return [costs[S] for S in sets]
+
+    (A0, M0), = q([()])
+    (C0,) = c([()])
+    tps0 = A0 / C0
+    cand = list(range(n_layers - latter_barrier - 1, early_barrier - 1, -1))
+    rank = lambda S: (-entries[S][0], -len(S), -entries[S][0] / costs[S])  # noqa: E731
+    beam, kept, per_depth = [()], [], []
+    while beam and (max_depth is None or len(per_depth) < max_depth):
+        children, seen = [], set()
+        for S in beam:
+            for l in cand:
+                if l in S:
+                    continue
+                ch = tuple(sorted(S + (l,)))
+                if ch not in seen:
+                    seen.add(ch)
+                    children.append(ch)
+        ok = [S for S, (A, M) in zip(children, q(children)) if A >= A0 and M >= (1 - score_tol) * M0]
+        per_depth.append(len(ok))
+        if log:
+            log(f"beam depth {len(per_depth)}: {len(children)} children, {len(ok)} kept")
+        if not ok:
+            break
+        c(ok)
+        kept.extend(ok)
+        beam = sorted(ok, key=rank)[:beam_width]
+    wins = [S for S in kept if entries[S][1] >= M0 and entries[S][0] >= A0 and entries[S][0] / costs[S] >= tps0]
+    need = min(min_skips, max((len(S) for S in kept), default=0))
+    pref = [S for S in wins if len(S) >= need] or wins
+    ranked = sorted(pref, key=rank)
+    best = ranked[0] if ranked else ()
+    pareto = [Entry(S, entries[S][0], entries[S][1], costs[S]) for S in ranked]
+    return SearchResult(best, Entry((), A0, M0, C0), pareto, kept, cand, per_depth,
+                        sum(1 for k in per_depth if k), len(entries), len(costs), entries, costs,
+                        time.perf_counter() - t0)
+
+
 # ---------------------------------------------------------------- GPU evaluators
 
 class SweepQuality:

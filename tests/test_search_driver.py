@@ -111,3 +111,40 @@ def test_candidate_layers_restrict_the_pool():
     res = breadth_search(L, 2, t.quality, t.cost, eps_A=1.0, eps_M=1.0, tau_A=1.0, tau_M=1.0, layers=[6, 2, 7])
     assert res.pool == [2, 6, 7]
     assert all(set(S) <= {2, 6, 7} for S in res.feasible)
+
+
+# ------------------------------------------------------------ the beam variant
+
+from paper_2609_26100_amd.search import beam_search  # noqa: E402
+
+
+def test_beam_worked_case():
+    """6 layers, barriers 2 / 0 (candidates 5, 4, 3, 2), beam 2.  Dense A 3.0,
+    M 0.80, C 10.  Depth 1 keeps {5} (3.2), {4} (3.0), {3} (3.1), {2} fails
+    A; beam {5}, {3}.  Depth 2 children of {5}: {4,5}, {3,5}, {2,5}; of {3}:
+    {3,4}, {2,3}: kept {3,5} (3.4), {4,5} (3.0; M 0.77 is within 5 %); beam
+    {3,5}, {4,5}.  Depth 3: {3,4,5} fails M, {2,3,5} fails A, {2,4,5} fails A:
+    stop.  Triple wins (M >= 0.80, A >= 3.0, A/C >= 0.3): {5}, {3}, {4},
+    {3,5}; {4,5} has M 0.77.  Largest kept set 2, so sets of >= 2 skips are
+    preferred: {3,5}."""
+    T = {(): (3.0, 0.80, 10.0), (5,): (3.2, 0.80, 9.0), (3,): (3.1, 0.81, 9.0), (4,): (3.0, 0.85, 9.0),
+         (2,): (2.9, 0.90, 9.0), (0,): (9.0, 0.90, 1.0), (1,): (9.0, 0.90, 1.0),
+         (4, 5): (3.0, 0.77, 8.0), (3, 5): (3.4, 0.80, 8.0), (2, 5): (2.0, 0.80, 8.0), (3, 4): (2.5, 0.80, 8.0),
+         (2, 3): (2.5, 0.80, 8.0), (3, 4, 5): (3.5, 0.70, 7.0), (2, 3, 5): (2.0, 0.80, 7.0),
+         (2, 4, 5): (2.0, 0.80, 7.0)}
+    t = Table(table_eval(_t(T)))
+    res = beam_search(6, t.quality, t.cost, beam_width=2, early_barrier=2, latter_barrier=0, score_tol=0.05)
+    assert res.pool == [5, 4, 3, 2]
+    assert res.per_depth == [3, 2, 0]
+    assert res.feasible == [(5,), (4,), (3,), (4, 5), (3, 5)]     # in the order met
+    assert res.best == (3, 5)
+    assert [e.skip for e in res.pareto] == [(3, 5), ]
+    assert all(0 not in S and 1 not in S for S in res.entries)   # the early barrier is never skipped
+    assert res.evaluations == 1 + 4 + 5 + 3
+
+
+def test_beam_without_a_triple_win_returns_dense():
+    T = {(): (3.0, 0.80, 10.0), (3,): (3.0, 0.79, 10.5)}     # kept (within 5 %) but neither M nor tok/s wins
+    t = Table(table_eval(_t(T)))
+    res = beam_search(4, t.quality, t.cost)
+    assert res.feasible == [(3,)] and res.best == () and res.pareto == []
