@@ -74,6 +74,29 @@ template <int MT, int NT, int S> struct Depth {
   static constexpr int v = raw < 1 ? 1 : (raw > 8 ? 8 : raw);
 };
 
+// dynamic LDS of the many-row variants: the CU's 160 KiB less room for the
+// kernel's static per-row arrays; the one-row-tile and narrow variants stay
+// within 64 KiB (measured faster)
+constexpr size_t kGemmLdsMax = 152 * 1024;
+template <int MT, int NT>
+constexpr size_t gemm_lds_cap() { return (MT == 1 || (MT <= 4 && NT <= 2)) ? 65536 : kGemmLdsMax; }
+
+// Cross-wave reduction in column passes of RC columns: the widest pass (a
+// multiple of 16 dividing the block's columns) for which the 8 waves'
+// partial tiles [8][ROWS][RC], the summed tile yfin [ROWS][COLS], the
+// residual epilogue's squares aux [ROWS][COLS] and the row scales fit the
+// LDS cap, so every variant keeps 8 waves.
+template <int MT, int NT>
+constexpr int red_cols() {
+  int cw = NT * 16;
+  while (cw > 16 && (size_t)(8 * MT * 16 * cw + 2 * MT * 16 * NT * 16 + MT * 16) * 4 > gemm_lds_cap<MT, NT>()) cw /= 2;
+  return cw;
+}
+template <int MT, int NT>
+constexpr size_t gemm_lds(int waves) {
+  return (size_t)(waves * MT * 16 * red_cols<MT, NT>() + 2 * MT * 16 * NT * 16 + MT * 16) * 4;
+}
+
 template <typename T, int MT, int NT, int EPI>
 __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
@@ -211,22 +234,14 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       if (i0 + D + j < n_my) compute(wv[j], xv[j]);
   }
 
-  // LDS: red[max(waves, 2)][ROWS][COLS] | rscale[ROWS].  The sum over waves
-  // lands in red's first slice (yfin: each element is read and written by
-  // one thread) and the residual epilogue's squares in its second (aux).
+  // LDS: red[waves][ROWS][RC] | yfin[ROWS][COLS] | aux[ROWS][COLS] | rscale[ROWS].
+  // The waves' partial tiles meet in red one pass of RC columns at a time;
+  // their sum lands in yfin, the residual epilogue's squares in aux.
+  constexpr int RC = red_cols<MT, NT>();
   float* red = smem;
-  float* yfin = red;
-  float* aux = red + ROWS * COLS;
-  float* rscale = red + (waves < 2 ? 2 : waves) * ROWS * COLS;
-
-  // MFMA result layout: lane holds column r16, rows 4*grp + v.
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        red[(wave * ROWS + mt * 16 + grp * 4 + v) * COLS + nt * 16 + r16] = acc[mt][nt][v];
+  float* yfin = red + waves * ROWS * RC;
+  float* aux = yfin + ROWS * COLS;
+  float* rscale = aux + ROWS * COLS;
 
   // RMSNorm row scale from the producer's partial sums (fixed order, so every
   // workgroup derives the same value): here when each row has its own wave
@@ -239,13 +254,25 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
     if (lane == 0) rscale[wave] = rsqrtf(s / (float)a.norm_dim + a.eps);
   }
-  __syncthreads();
 
-  for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
-    const int row = e / COLS, col = e % COLS;
-    float s = 0.f;
-    for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * COLS + col];
-    yfin[row * COLS + col] = s;
+  // MFMA result layout: lane holds column r16, rows 4*grp + v.
+#pragma unroll
+  for (int c0 = 0; c0 < COLS; c0 += RC) {
+    if (c0 > 0) __syncthreads();  // the previous pass has read red
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = c0 / 16; nt < (c0 + RC) / 16; ++nt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          red[(wave * ROWS + mt * 16 + grp * 4 + v) * RC + nt * 16 - c0 + r16] = acc[mt][nt][v];
+    __syncthreads();
+    for (int e = threadIdx.x; e < M * RC; e += blockDim.x) {
+      const int row = e / RC, col = e % RC;
+      float s = 0.f;
+      for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * RC + col];
+      yfin[row * COLS + c0 + col] = s;
+    }
   }
 
   if (!ss_early) {
@@ -368,14 +395,6 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   }
 }
 
-// dynamic LDS of the many-row variants: the CU's 160 KiB less room for the
-// kernel's static per-row arrays
-constexpr size_t kGemmLdsMax = 152 * 1024;
-
-template <int MT, int NT>
-constexpr size_t gemm_lds(int waves) {
-  return (size_t)((waves < 2 ? 2 : waves) * MT * 16 * NT * 16 + MT * 16) * 4;
-}
 
 template <typename T, int MT, int NT, int EPI>
 static hipError_t gemm_attr() {
@@ -423,7 +442,7 @@ static hipError_t launch_v(const GemmArgs& a, hipStream_t s) {
   // 8 waves (measured best across the 7B shapes) unless K is short, capped by
   // LDS: up to 64 rows the cross-wave reduction stays within 64 KiB
   // (4-tile blocks and more than 4 row tiles may use most of the CU's LDS)
-  const size_t cap = (MT == 1 || (MT <= 4 && NT <= 2)) ? 65536 : kGemmLdsMax;
+  const size_t cap = gemm_lds_cap<MT, NT>();
   int waves = a.nkc < 8 ? a.nkc : 8;
   while (waves > 1 && gemm_lds<MT, NT>(waves) > cap) waves >>= 1;
   const size_t lds = gemm_lds<MT, NT>(waves);
