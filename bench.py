@@ -74,7 +74,7 @@ def batch_bytes(shape, seqs):
 # the traffic field until the counters are taken again.
 GATEUP_COUNTERS = {"fetch_kib": 88652.5, "write_kib": 258.0, "fetch_scale": 2.0, "write_scale": 1.0,
                    "sources": ("paper_2609_26100_amd/csrc/k_gemm.hip", "paper_2609_26100_amd/csrc/tss_internal.h"),
-                   "sha256": "c107ec1c6468146a247b1d8f5ab9bebbd7d588afbf95340d0c36fdf71981cf6e"}
+                   "sha256": "1013c3784c286411776b1aef0be1c6c2c8bb0cea47d497beb05aa4cd2b1920ea"}
 
 
 def gateup_traffic():
