@@ -121,3 +121,29 @@ def test_skip_mask_equals_deleted_blocks(gpu):
     assert a == b
     np.testing.assert_array_equal(v.logits(6), w.logits(6))
     w.close()
+
+
+def _paper_7b_sets():
+    import json
+    import os
+    rows = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_table1_skip_sets.json")))["rows"]
+    return [(r["domain"], r["skip"]) for r in rows if r["n_layers"] == L]
+
+
+@pytest.mark.parametrize("domain,skip", _paper_7b_sets())
+def test_paper_skip_sets(gpu, domain, skip):
+    """The skip sets the paper reports for the 7B target (Table 1), at the
+    benchmark's context: prefill under the set, the target's own greedy drafts
+    fully accepted, repeated steps bit-exact."""
+    v = gpu
+    root = _prepare(v, synth.mask_from_layers(L, skip))
+    cur = [root]
+    for _ in range(6):
+        v.verify(0, cur)
+        cur.append(int(v.greedy(len(cur))[-1]))
+    al, nt = v.verify(0, cur[:6])
+    first = v.logits(6)
+    assert (al, nt) == (5, cur[6])
+    assert v.verify(0, cur[:6]) == (al, nt)
+    np.testing.assert_array_equal(v.logits(6), first)
+    log(f"paper skip set {domain} {skip}: own greedy chain fully accepted")
