@@ -380,14 +380,15 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       const int row = e / COLS, col = e % COLS;
       a.logits[(size_t)row * N + n0 + col] = yfin[row * COLS + col];
     }
-    // one (max, argmax) per 16 columns, lowest column on ties
+    // one (max, argmax) per 16 columns, lowest column on ties; NaN counts as
+    // the largest value (first NaN wins), as in numpy's argmax
     for (int e = threadIdx.x; e < M * NT; e += blockDim.x) {
       const int row = e / NT, j = e % NT;
       float bv = yfin[row * COLS + j * 16];
       int bi = j * 16;
       for (int col = j * 16 + 1; col < j * 16 + 16; ++col) {
         const float v = yfin[row * COLS + col];
-        if (v > bv) { bv = v; bi = col; }
+        if (__builtin_isnan(v) ? !__builtin_isnan(bv) : v > bv) { bv = v; bi = col; }
       }
       a.am_val[(size_t)row * a.am_stride + strip * NT + j] = bv;
       a.am_idx[(size_t)row * a.am_stride + strip * NT + j] = n0 + bi;

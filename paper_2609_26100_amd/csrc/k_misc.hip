@@ -80,8 +80,11 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
 }
 
 // (value, index) order of the greedy argmax: larger value first, lower index on ties.
+// NaN counts as the largest value (the lowest index among NaNs), as numpy's
+// argmax has it, so a row with NaN logits still yields an in-range token.
 __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
-  return v > bv || (v == bv && i < bi);
+  const bool nv = __builtin_isnan(v), nb = __builtin_isnan(bv);
+  return (nv && !nb) || v > bv || ((v == bv || (nv && nb)) && i < bi);
 }
 
 // One workgroup of 16 waves.  Greedy token per row from the lm_head's

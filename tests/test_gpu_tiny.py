@@ -291,3 +291,55 @@ def test_committing_decode_loop(pair, mode):
             break
     assert steps >= 6
     v.set_launch_mode(abi.TSS_LAUNCH_GRAPH)
+
+
+def test_nan_logits_pick_the_first_nan():
+    """Degenerate logits: lm_head rows 17 and 3000 hold NaN, so those two
+    logits are NaN for every node.  The greedy token is then the first NaN
+    index, as in the oracle's (numpy's) argmax, and never an out-of-range
+    index: every node's greedy token is 17, a chain of 17s is fully
+    accepted and the bonus token is 17."""
+    from paper_2609_26100_amd.verifier import Verifier
+
+    names = {i: (layer, nm) for i, layer, nm in synth.tensor_names(L)}
+    base = synth.abi_tensor_loader(SHAPE)
+
+    def poisoned(a):
+        a = np.array(a, copy=True)
+        a[[17, 3000]] = np.nan
+        return a
+
+    def get(index):
+        a = base(index)
+        return poisoned(a) if names[index][1] == "lm_head" else a
+
+    ocache = {}
+
+    def oget(name, layer):
+        if (name, layer) not in ocache:
+            t = synth.weight_tensor(SHAPE, name, layer)
+            ocache[(name, layer)] = poisoned(t) if name == "lm_head" else t
+        return ocache[(name, layer)]
+
+    from oracle import OracleModel
+    v = Verifier(SHAPE, n_seqs=1, max_tokens=128, max_nodes=16)
+    try:
+        v.load(get)
+        m = OracleModel(SHAPE, oget)
+        ctx = synth.context_tokens(SHAPE.vocab, 30, stream=77)
+        v.prefill(0, ctx)
+        o = OracleSequence(m, None)
+        prefill(m, o, ctx)
+        tok = np.array([5, 17, 17, 17, 17, 17], np.int32)
+        res = verify(m, o, tok)
+        al, nt = v.verify(0, tok)
+        g = v.greedy(len(tok))
+        lg = v.logits(len(tok))
+        assert np.isnan(lg[:, [17, 3000]]).all() and np.isnan(res.logits[:, [17, 3000]]).all()
+        np.testing.assert_array_equal(res.greedy, np.full(len(tok), 17))
+        np.testing.assert_array_equal(g, np.full(len(tok), 17))
+        assert (al, nt) == (res.accept_len, res.next_token) == (5, 17)
+        finite = np.isfinite(res.logits)
+        assert float(np.max(np.abs(lg[finite] - res.logits[finite]))) <= 1e-4
+    finally:
+        v.close()
