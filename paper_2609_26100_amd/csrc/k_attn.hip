@@ -80,7 +80,46 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   constexpr int OS = NO * 4 + 1;
 
   const int head = blockIdx.x, y = blockIdx.y, g = blockIdx.z;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r16 = lane & 15, grp = lane >> 4;
+  // The wave index is uniform, so page ids and page addresses come from
+  // scalar loads, whose waits never hold back page loads in flight.
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63, r16 = lane & 15,
+            grp = lane >> 4;
+  const int arg_pages = a.n_arg_pages;
+  const int32_t* pt = a.page_table;  // this item's row of the page table, set below
+
+  const size_t blk_elems = 16 * (size_t)HD;
+  auto load_phys = [&](int phys, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
+    const TK* kb = (const TK*)a.kv_pages + (((size_t)a.layer * a.n_pages_pool + phys) * 2 * a.n_heads + head) * blk_elems;
+    const TK* vb = kb + (size_t)a.n_heads * blk_elems;
+    const uint4* kp = (const uint4*)(kb + r16 * HD + grp * DL);
+    const uint4* vp = (const uint4*)(vb + grp * HD * 4 + r16 * NO * 4);
+#pragma unroll
+    for (int c = 0; c < NQ; ++c) kreg[c] = kp[c];
+#pragma unroll
+    for (int c = 0; c < NV; ++c) vreg[c] = vp[c];
+  };
+  // Page p of the item's sequence.  p is uniform: the argument list is read
+  // with a scalar load, and only pages past it read the page table (a
+  // uniform branch, so that read's wait never holds back an argument page).
+  auto load_page = [&](int p, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
+    int phys;
+    if (p < arg_pages)
+      phys = a.pages[p];
+    else
+      phys = __builtin_amdgcn_readfirstlane(__builtin_nontemporal_load(pt + p));
+    load_phys(phys, kreg, vreg);
+  };
+
+  // The wave's first page is requested before anything else when its id is
+  // an argument: every argument id names a page of the pool, so the load is
+  // in bounds even if the page lies past the context (its data is then never
+  // used).  Its latency overlaps the reads of the item's parameters, q and
+  // the tree masks below.
+  uint4 kcur[NQ], vcur[NV];
+  int p = g * W + wave;
+  const bool early = p < arg_pages;
+  if (early) load_phys(a.pages[p], kcur, vcur);
+
   const int sq = a.item_seg[y];
   const int n_kv = a.sp->seq_nkv[sq];
   const int row0 = a.item_row0[y];
@@ -90,29 +129,38 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   // workgroups of this item: at most groups, at least a page per wave, and
   // few enough that partial states (T tiles each) stay well below the pages
   const int G = max(1, min(a.groups, min((n_pages + W - 1) / W, n_pages / (TSS_ATTN_PART_DIV * T))));
-  if (g >= G) return;                                // uniform over the workgroup
-  const int32_t* pt = a.page_table + a.pt_off[sq];
-  const int arg_pages = a.n_arg_pages;
+  if (g >= G) {                                      // uniform over the workgroup
+    __builtin_amdgcn_s_waitcnt(0);                   // let the early page load land first
+    return;
+  }
+  pt = a.page_table + a.pt_off[sq];
 
   // B operand of S = K Q^T for tile t: lane (node 16 t + r16, group grp)
   // holds q[node][head*HD + grp*DL + 0..DL).  Waves 0..T-1 build one tile
-  // each in LDS; every wave re-reads them per page.
+  // each in LDS (all of a lane's loads issued before the first conversion);
+  // every wave re-reads them per page.
   extern __shared__ float smem[];
   uint4* sm_q = (uint4*)smem;  // [TMAX][64][NQ]
   if (wave < T) {
     const int ln = wave * 16 + r16;  // local node
     const float* qrow = a.q + (size_t)(row0 + ln) * a.d + head * HD + grp * DL;
+    constexpr int NF = DL / 4;       // float4 loads per lane
+    float4 f[NF];
+    if (ln < Ms) {
+#pragma unroll
+      for (int i = 0; i < NF; ++i) f[i] = *(const float4*)(qrow + i * 4);
+    } else {
+#pragma unroll
+      for (int i = 0; i < NF; ++i) f[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
 #pragma unroll
     for (int c = 0; c < NQ; ++c) {
-      uint4 qv = uint4{0, 0, 0, 0};
-      if (ln < Ms) {
-        if constexpr (sizeof(TK) == 2) {
-          const float4 f0 = *(const float4*)(qrow + c * 8);
-          const float4 f1 = *(const float4*)(qrow + c * 8 + 4);
-          qv = uint4{pack_f16x2(f0.x, f0.y), pack_f16x2(f0.z, f0.w), pack_f16x2(f1.x, f1.y), pack_f16x2(f1.z, f1.w)};
-        } else {
-          qv = *(const uint4*)(qrow + c * 4);
-        }
+      uint4 qv;
+      if constexpr (sizeof(TK) == 2) {
+        const float4 f0 = f[2 * c], f1 = f[2 * c + 1];
+        qv = uint4{pack_f16x2(f0.x, f0.y), pack_f16x2(f0.z, f0.w), pack_f16x2(f1.x, f1.y), pack_f16x2(f1.z, f1.w)};
+      } else {
+        qv = __builtin_bit_cast(uint4, f[c]);
       }
       sm_q[(wave * 64 + lane) * NQ + c] = qv;
     }
@@ -126,7 +174,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     const int ln = t * 16 + r16;
     const bool in = t < T && ln < Ms;
     anc[t] = in ? a.sp->anc[row0 + ln] : 0ull;
-    base[t] = in ? (int)a.sp->seg_slot0[a.sp->row_seq[row0 + ln]] : 0;
+    base[t] = in ? (int)a.sp->row_slot0[row0 + ln] : 0;
   }
 
   float m_run[TMAX], l_run[TMAX];
@@ -139,23 +187,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     for (int n = 0; n < NO; ++n) O[t][n] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  const size_t blk_elems = 16 * (size_t)HD;
-  auto load_page = [&](int p, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
-    const int phys = p < arg_pages ? a.pages[p] : pt[p];  // p is uniform across the wave
-    const TK* kb = (const TK*)a.kv_pages + (((size_t)a.layer * a.n_pages_pool + phys) * 2 * a.n_heads + head) * blk_elems;
-    const TK* vb = kb + (size_t)a.n_heads * blk_elems;
-    const uint4* kp = (const uint4*)(kb + r16 * HD + grp * DL);
-    const uint4* vp = (const uint4*)(vb + grp * HD * 4 + r16 * NO * 4);
-#pragma unroll
-    for (int c = 0; c < NQ; ++c) kreg[c] = kp[c];
-#pragma unroll
-    for (int c = 0; c < NV; ++c) vreg[c] = vp[c];
-  };
-
-  uint4 kcur[NQ], vcur[NV];
   const int stride = W * G;
-  int p = g * W + wave;
-  if (p < n_pages) load_page(p, kcur, vcur);
+  if (!early && p < n_pages) load_page(p, kcur, vcur);
   __syncthreads();  // q tiles ready
   for (; p < n_pages; p += stride) {
     uint4 knext[NQ], vnext[NV];

@@ -751,10 +751,10 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
         if (n_act == kAttnMaxItems) return fail(c, TSS_EINVAL, "too many attention items in one step");
         const int rows = std::min(64, hi - r);
         const int last_seg = sp.row_seq[r + rows - 1];
-        at.item_row0[n_act] = (uint8_t)r;
-        at.item_rows[n_act] = (uint8_t)rows;
+        at.item_row0[n_act] = r;
+        at.item_rows[n_act] = rows;
         at.item_seg[n_act] = sp.row_seq[r];
-        at.item_slots[n_act] = (uint8_t)(sp.seg_slot0[last_seg] + sp.seq_row0[last_seg + 1] - sp.seq_row0[last_seg]);
+        at.item_slots[n_act] = sp.seg_slot0[last_seg] + sp.seq_row0[last_seg + 1] - sp.seq_row0[last_seg];
         max_tiles = std::max(max_tiles, (rows + 15) / 16);
         ++n_act;
       }
@@ -1119,6 +1119,7 @@ int verify_batch(tss_ctx* c, int32_t n_seqs, const int32_t* seq_ids, const int32
       sp.depth[r0 + j] = (uint8_t)depth[j];
       sp.anc[r0 + j] = anc[j];
       sp.row_seq[r0 + j] = (uint8_t)i;
+      sp.row_slot0[r0 + j] = sp.seg_slot0[i];
     }
     st.compact[i] = commit && !chain;
   }
@@ -1231,6 +1232,7 @@ int verify_sweep(tss_ctx* c, int32_t seq, const int32_t* tokens, const int32_t* 
         sp.depth[r0 + j] = (uint8_t)depth[j];
         sp.anc[r0 + j] = anc[j];
         sp.row_seq[r0 + j] = (uint8_t)i;
+        sp.row_slot0[r0 + j] = (uint8_t)r0;
       }
     }
     sp.seq_row0[P] = P * n;

@@ -114,6 +114,7 @@ struct StepParams {
   uint8_t depth[kMaxRows];
   uint8_t row_seq[kMaxRows];       // segment (0 .. n_seqs-1) of the row
   uint8_t seg_slot0[kMaxSegs];     // first draft slot of each segment, after its sequence's context
+  uint8_t row_slot0[kMaxRows];     // seg_slot0 of the row's segment
 };
 
 // Position of a row: its sequence's committed length plus its depth.
@@ -192,10 +193,11 @@ struct AttnArgs {
   int groups;              // most workgroups per (head, item)
   int layer, n_pages_pool, n_heads, d;
   float scale_log2;        // log2(e) / sqrt(hd)
-  uint8_t item_row0[kAttnMaxItems];   // first row of the item
-  uint8_t item_rows[kAttnMaxItems];   // rows (1 .. 64)
-  uint8_t item_seg[kAttnMaxItems];    // segment of the first row (context length, page table)
-  uint8_t item_slots[kAttnMaxItems];  // draft slots after the context that its rows may see
+  // per item, 32-bit so that the kernel reads them with scalar loads
+  int32_t item_row0[kAttnMaxItems];   // first row of the item
+  int32_t item_rows[kAttnMaxItems];   // rows (1 .. 64)
+  int32_t item_seg[kAttnMaxItems];    // segment of the first row (context length, page table)
+  int32_t item_slots[kAttnMaxItems];  // draft slots after the context that its rows may see
   int32_t pt_off[kMaxSegs];
   int32_t n_arg_pages;     // with one KV sequence in the step: valid entries of pages[] (else 0)
   int32_t pages[kArgPages];  // physical ids of that sequence's first pages
