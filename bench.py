@@ -74,7 +74,7 @@ def batch_bytes(shape, seqs):
 # the traffic field until the counters are taken again.
 GATEUP_COUNTERS = {"fetch_kib": 88652.5, "write_kib": 258.0, "fetch_scale": 2.0, "write_scale": 1.0,
                    "sources": ("paper_2609_26100_amd/csrc/k_gemm.hip", "paper_2609_26100_amd/csrc/tss_internal.h"),
-                   "sha256": "1013c3784c286411776b1aef0be1c6c2c8bb0cea47d497beb05aa4cd2b1920ea"}
+                   "sha256": "148b684a39fb5daac5599358aad249caef397d672d0b74a968465d61d5fd2d13"}
 
 
 def gateup_traffic():
