@@ -64,13 +64,17 @@ __device__ __forceinline__ uint4 load_stream(const uint8_t* p) {
 
 // Chunks each wave keeps in flight: a ring of D slots, each holding one
 // chunk's weight tiles (NT x 4 VGPRs) and activation tiles (MT x S x 4
-// VGPRs), sized to about 160 VGPRs per lane.
-// (64 VGPRs with one row tile, where more would cost occupancy, and with the
-// largest accumulator sets (20+ tiles), where more would spill; 128 between;
-// measured on the 7B projections)
-template <int MT, int NT, int S> struct Depth {
+// VGPRs), sized to a VGPR budget per lane: 64 with one row tile, where more
+// would cost occupancy, and with the largest accumulator sets (20+ tiles),
+// where more would spill; 128 between.  The one-row-tile gate/up takes 32
+// (two slots): its many workgroups then fit three to a CU, and with that many
+// waves a shallower ring streams faster (7B k=5 step 3168 -> 3138 us; deeper
+// rings for the other one-row-tile projections measured slower).  Measured
+// on the 7B projections.
+template <int MT, int NT, int S, int EPI> struct Depth {
   static constexpr int per = NT * 4 + MT * S * 4;
-  static constexpr int raw = (MT == 1 || MT * NT >= 20 ? 64 : 128) / per;
+  static constexpr int budget = MT == 1 ? (EPI == EPI_SWIGLU ? 32 : 64) : (MT * NT >= 20 ? 64 : 128);
+  static constexpr int raw = budget / per;
   static constexpr int v = raw < 1 ? 1 : (raw > 8 ? 8 : raw);
 };
 
@@ -102,7 +106,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
   constexpr int KL = KC / 4;           // K elements per lane per tile
   constexpr int S = Mode<T>::planes;
-  constexpr int D = Depth<MT, NT, S>::v;
+  constexpr int D = Depth<MT, NT, S, EPI>::v;
   using KV = typename Mode<T>::KV;
   constexpr int ROWS = MT * 16;
   constexpr int COLS = NT * 16;
