@@ -92,9 +92,10 @@ constexpr size_t gemm_lds_cap() { return (MT == 1 || (MT <= 4 && NT <= 2)) ? 655
 // LDS cap, so every variant keeps 8 waves.
 template <int MT, int NT>
 constexpr int red_cols() {
-  int cw = NT * 16;
-  while (cw > 16 && (size_t)(8 * MT * 16 * cw + 2 * MT * 16 * NT * 16 + MT * 16) * 4 > gemm_lds_cap<MT, NT>()) cw /= 2;
-  return cw;
+  for (int t = NT; t > 1; --t)
+    if (NT % t == 0 && (size_t)(8 * MT * 16 * (16 * t) + 2 * MT * 16 * NT * 16 + MT * 16) * 4 <= gemm_lds_cap<MT, NT>())
+      return 16 * t;
+  return 16;
 }
 template <int MT, int NT>
 constexpr size_t gemm_lds(int waves) {
@@ -423,6 +424,9 @@ static hipError_t gemm_attr_rows() {
   hipError_t e = gemm_attr_mt<T, MT, 1>();
   if (e == hipSuccess) e = gemm_attr_mt<T, MT, 2>();
   if (e == hipSuccess) e = gemm_attr_mt<T, MT, 4>();
+  if (e == hipSuccess) e = gemm_attr<T, MT, 3, EPI_QKV>();  // three-tile blocks: Q/K/V only
+  if constexpr (MT >= 2 && MT <= 4)  // eight-tile gate/up blocks (four pairs)
+    if (e == hipSuccess) e = gemm_attr<T, MT, 8, EPI_SWIGLU>();
   return e;
 }
 
@@ -474,6 +478,10 @@ static hipError_t launch_rows(int epi, int nt, const GemmArgs& a, hipStream_t s)
     case 1: return launch_mt<T, MT, 1>(epi, a, s);
     case 2: return launch_mt<T, MT, 2>(epi, a, s);
     case 4: return launch_mt<T, MT, 4>(epi, a, s);
+    case 3: return epi == EPI_QKV ? launch_v<T, MT, 3, EPI_QKV>(a, s) : hipErrorInvalidValue;
+    case 8:
+      if constexpr (MT >= 2 && MT <= 4) return epi == EPI_SWIGLU ? launch_v<T, MT, 8, EPI_SWIGLU>(a, s) : hipErrorInvalidValue;
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }

@@ -282,12 +282,25 @@ hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base,
 // matrix in one round of at most 256 workgroups (with more than one row tile
 // a workgroup fills a CU), except that with one row tile gate/up keeps one
 // gate/up pair, lm_head one tile, and Q/K/V takes 4 tiles only if that fits
-// 256 workgroups (else 2).  (Splitting K over workgroups to widen the blocks
+// 256 workgroups (else 2), and Q/K/V takes 3 tiles when that gives more than
+// 192 and at most 256 workgroups (7B: 256 instead of 192; the 7B k=5 step
+// 3133 -> 3096 us, the 60-node tree 5903 -> 5792 us); with 2-4 row tiles
+// gate/up takes 8 tiles when they fit 256 workgroups (the 60-node tree
+// 5851 -> 5531 us; with 5 row tiles they spill and the 13B batch slows).
+// (Splitting K over
+// workgroups to widen the blocks
 // further measured slower: partial sums and a device-scope fence per
 // workgroup.)
 inline int gemm_tiles(int epi, int mt, int N) {
+  // gate/up with 2-4 row tiles: eight-tile blocks (four pairs) when they fit
+  // one round (7B: 172 workgroups instead of 344 in 1.34 rounds; more row
+  // tiles would spill)
+  if (epi == EPI_SWIGLU && mt >= 2 && mt <= 4 && N % 128 == 0 && N / 128 <= 256) return 8;
   if (epi == EPI_SWIGLU) return (mt == 1 || N % 64) ? 2 : 4;
   if (mt == 1 && epi == EPI_LOGITS) return 1;
+  // three-tile Q/K/V blocks where they fill one round better than four-tile
+  // ones can (more than 192 and at most 256 workgroups: the 7B shape's 256)
+  if (epi == EPI_QKV && N % 48 == 0 && N / 48 <= 256 && N / 48 > 192) return 3;
   if (mt == 1 && epi == EPI_QKV) return (N % 64 == 0 && N / 64 <= 256) ? 4 : (N % 32 == 0 ? 2 : 1);
   for (int nt = 1; nt <= 4; nt *= 2)
     if (N % (16 * nt) == 0 && N / (16 * nt) <= 256) return nt;
