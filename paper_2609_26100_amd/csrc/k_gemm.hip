@@ -427,6 +427,10 @@ static hipError_t gemm_attr_rows() {
   if (e == hipSuccess) e = gemm_attr<T, MT, 3, EPI_QKV>();  // three-tile blocks: Q/K/V only
   if constexpr (MT >= 2 && MT <= 4)  // eight-tile gate/up blocks (four pairs)
     if (e == hipSuccess) e = gemm_attr<T, MT, 8, EPI_SWIGLU>();
+  if constexpr (MT >= 2 && MT <= 4)  // six-tile Q/K/V blocks
+    if (e == hipSuccess) e = gemm_attr<T, MT, 6, EPI_QKV>();
+  if constexpr (MT >= 2 && MT <= 3)  // ten-tile gate/up blocks (five pairs)
+    if (e == hipSuccess) e = gemm_attr<T, MT, 10, EPI_SWIGLU>();
   return e;
 }
 
@@ -481,6 +485,12 @@ static hipError_t launch_rows(int epi, int nt, const GemmArgs& a, hipStream_t s)
     case 3: return epi == EPI_QKV ? launch_v<T, MT, 3, EPI_QKV>(a, s) : hipErrorInvalidValue;
     case 8:
       if constexpr (MT >= 2 && MT <= 4) return epi == EPI_SWIGLU ? launch_v<T, MT, 8, EPI_SWIGLU>(a, s) : hipErrorInvalidValue;
+      return hipErrorInvalidValue;
+    case 6:
+      if constexpr (MT >= 2 && MT <= 4) return epi == EPI_QKV ? launch_v<T, MT, 6, EPI_QKV>(a, s) : hipErrorInvalidValue;
+      return hipErrorInvalidValue;
+    case 10:
+      if constexpr (MT >= 2 && MT <= 3) return epi == EPI_SWIGLU ? launch_v<T, MT, 10, EPI_SWIGLU>(a, s) : hipErrorInvalidValue;
       return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
