@@ -312,22 +312,34 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     }
     __syncthreads();
 
-    // Output position e = (source lane, n, v): node row 4*(lane/16)+v of the
-    // tile, dim NO*(lane%16)+n; its value is sum_w f_w O_w (unnormalised).
+    // Output (source lane src, row v of its four, tiles n0 .. n0+3): node row
+    // 4*(src/16)+v of the tile, dims NO*(src%16)+n0 .. +3 (contiguous, so one
+    // vector store each); value sum_w f_w O_w (unnormalised), in wave order.
+    static_assert(NO % 4 == 0, "four output tiles per store");
     float* pm = a.part_ml + (slot * TMAX + t) * 32;      // [16][2]
     float* po = a.part_o + (slot * TMAX + t) * 16 * HD;  // [16][HD]
-    for (int e = threadIdx.x; e < 64 * NO * 4; e += blockDim.x) {
-      const int src = e / (NO * 4), n = (e / 4) % NO, v = e % 4;
+    for (int e = threadIdx.x; e < 64 * NO; e += blockDim.x) {
+      const int src = e / NO, v = (e / (NO / 4)) % 4, n0 = (e % (NO / 4)) * 4;
       const int row = (src >> 4) * 4 + v;
       const int ln = t * 16 + row;
       if (ln >= Ms) continue;
-      float num = 0.f;
-      for (int w = 0; w < W; ++w) num += sm_f[w * 16 + row] * sm_o[(w * 64 + src) * OS + n * 4 + v];
-      const int dim = NO * (src & 15) + n;
-      if (G == 1)
-        store_act<TW>(a.o, a.o_plane, act_index<TW>(row0 + ln, head * HD + dim, a.d), num / sm_den[row]);
-      else
-        po[row * HD + dim] = num;
+      float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int w = 0; w < W; ++w) {
+        const float f = sm_f[w * 16 + row];
+        const float* so = sm_o + (w * 64 + src) * OS + n0 * 4 + v;
+        num.x += f * so[0];
+        num.y += f * so[4];
+        num.z += f * so[8];
+        num.w += f * so[12];
+      }
+      const int dim = NO * (src & 15) + n0;
+      if (G == 1) {
+        const float den = sm_den[row];
+        store_act4<TW>(a.o, a.o_plane, act_index<TW>(row0 + ln, head * HD + dim, a.d),
+                       make_float4(num.x / den, num.y / den, num.z / den, num.w / den));
+      } else {
+        *(float4*)(po + row * HD + dim) = num;
+      }
     }
     if (G > 1 && threadIdx.x < 16) {
       pm[threadIdx.x * 2 + 0] = sm_mx[threadIdx.x];
@@ -354,18 +366,66 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   if (!last) return;
   // Phase 1: per (tile, row) the normalised weight of each partial,
   // w_k = 2^(m_k - max m) / sum_k 2^(m_k - max m) l_k, into LDS (the q tiles
-  // are no longer needed).  Phase 2: each thread merges 4 dims, with all G
-  // loads issued together (the index is clamped and the weight is 0 past G).
+  // are no longer needed).  Phase 2: each thread merges 4 dims of up to R
+  // outputs per round (two with several row tiles; one with a single tile,
+  // where each thread has one output and the registers stay within what two
+  // workgroups per CU allow), reading only the G partials (summed in
+  // workgroup order); the first round's loads are issued before phase 1, so
+  // the two round trips overlap.
   const size_t slot0 = ((size_t)head * gridDim.y + y) * a.groups;
   float* sm_w = smem;  // [T * 16][kAttnMaxGroups]
+  const int n_e4 = T * 4 * HD;
+  const size_t part_stride = (size_t)TMAX * 16 * HD;  // floats between consecutive partial slots
+  constexpr int R = TMAX >= 2 ? 2 : 1;
+  float4 v[R][kAttnMaxGroups];
+  auto load_round = [&](int base) {
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      // clamped, so every load stays inside the item's partials; the
+      // clamped outputs are not stored
+      const int e4 = min(base + i * (int)blockDim.x + (int)threadIdx.x, n_e4 - 1);
+      const int e = e4 * 4;
+      const int t = e / (16 * HD), row = (e / HD) % 16, dim = e % HD;
+      const float* src = a.part_o + (slot0 * TMAX + t) * 16 * HD + row * HD + dim;
+#pragma unroll
+      for (int k = 0; k < kAttnMaxGroups; ++k)
+        if (k < G) v[i][k] = *(const float4*)(src + k * part_stride);
+    }
+  };
+  auto merge_round = [&](int base) {
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const int e4 = base + i * (int)blockDim.x + (int)threadIdx.x;
+      if (e4 >= n_e4) continue;
+      const int e = e4 * 4;
+      const int t = e / (16 * HD), row = (e / HD) % 16, dim = e % HD;
+      const int ln = t * 16 + row;
+      if (ln >= Ms) continue;
+      const float* w = sm_w + (t * 16 + row) * kAttnMaxGroups;
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int k = 0; k < kAttnMaxGroups; ++k) {
+        if (k < G) {
+          acc.x += w[k] * v[i][k].x;
+          acc.y += w[k] * v[i][k].y;
+          acc.z += w[k] * v[i][k].z;
+          acc.w += w[k] * v[i][k].w;
+        }
+      }
+      store_act4<TW>(a.o, a.o_plane, act_index<TW>(row0 + ln, head * HD + dim, a.d), acc);
+    }
+  };
+  load_round(0);
   for (int idx = threadIdx.x; idx < T * 16; idx += blockDim.x) {
     const int t = idx >> 4, row = idx & 15;
+    const float* pm = a.part_ml + (slot0 * TMAX + t) * 32 + row * 2;
     float mk[kAttnMaxGroups], lk[kAttnMaxGroups];
 #pragma unroll
     for (int k = 0; k < kAttnMaxGroups; ++k) {
-      const float* pm = a.part_ml + ((slot0 + min(k, G - 1)) * TMAX + t) * 32 + row * 2;
-      mk[k] = pm[0];
-      lk[k] = pm[1];
+      if (k < G) {
+        mk[k] = pm[k * TMAX * 32];
+        lk[k] = pm[k * TMAX * 32 + 1];
+      }
     }
     float mx = -1e30f;
 #pragma unroll
@@ -375,36 +435,17 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int k = 0; k < kAttnMaxGroups; ++k) {
       f[k] = k < G ? exp2f(mk[k] - mx) : 0.f;
-      den += f[k] * lk[k];
+      if (k < G) den += f[k] * lk[k];
     }
     const float inv = 1.f / den;
 #pragma unroll
     for (int k = 0; k < kAttnMaxGroups; ++k) sm_w[idx * kAttnMaxGroups + k] = f[k] * inv;
   }
   __syncthreads();
-  for (int e4 = threadIdx.x; e4 < T * 4 * HD; e4 += blockDim.x) {
-    const int e = e4 * 4;
-    const int t = e / (16 * HD), row = (e / HD) % 16, dim = e % HD;
-    const int ln = t * 16 + row;
-    if (ln >= Ms) continue;
-    float4 v[kAttnMaxGroups];
-#pragma unroll
-    for (int k = 0; k < kAttnMaxGroups; ++k)
-      v[k] = *(const float4*)(a.part_o + ((slot0 + min(k, G - 1)) * TMAX + t) * 16 * HD + row * HD + dim);
-    const float* w = sm_w + (t * 16 + row) * kAttnMaxGroups;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int k = 0; k < kAttnMaxGroups; ++k) {
-      acc.x += w[k] * v[k].x;
-      acc.y += w[k] * v[k].y;
-      acc.z += w[k] * v[k].z;
-      acc.w += w[k] * v[k].w;
-    }
-    const int node = row0 + ln;
-    store_act<TW>(a.o, a.o_plane, act_index<TW>(node, head * HD + dim + 0, a.d), acc.x);
-    store_act<TW>(a.o, a.o_plane, act_index<TW>(node, head * HD + dim + 1, a.d), acc.y);
-    store_act<TW>(a.o, a.o_plane, act_index<TW>(node, head * HD + dim + 2, a.d), acc.z);
-    store_act<TW>(a.o, a.o_plane, act_index<TW>(node, head * HD + dim + 3, a.d), acc.w);
+  merge_round(0);
+  for (int base = R * (int)blockDim.x; base < n_e4; base += R * (int)blockDim.x) {
+    load_round(base);
+    merge_round(base);
   }
   if (threadIdx.x == 0) a.counters[ctr] = 0;
 }

@@ -95,6 +95,22 @@ __device__ __forceinline__ void store_act(void* base, size_t plane, size_t idx, 
   }
 }
 
+// Stores activations k .. k+3 of one row (k a multiple of 4), which act_index
+// places next to each other in each plane: one 8-byte (bf16 planes) or 16-byte
+// (f32) store per plane instead of one per element.  idx = act_index(row, k).
+template <typename T>
+__device__ __forceinline__ void store_act4(void* base, size_t plane, size_t idx, float4 v) {
+  if constexpr (Mode<T>::planes == 2) {
+    const T h0 = (T)v.x, h1 = (T)v.y, h2 = (T)v.z, h3 = (T)v.w;
+    const T l0 = (T)(v.x - (float)h0), l1 = (T)(v.y - (float)h1), l2 = (T)(v.z - (float)h2), l3 = (T)(v.w - (float)h3);
+    typedef T t4 __attribute__((ext_vector_type(4)));
+    *(t4*)((T*)base + idx) = t4{h0, h1, h2, h3};
+    *(t4*)((T*)base + plane + idx) = t4{l0, l1, l2, l3};
+  } else {
+    *(float4*)((T*)base + idx) = v;
+  }
+}
+
 // Per-step data that changes from step to step (tokens, tree, context
 // lengths).  Rows are grouped into segments: the nodes of one draft tree
 // verified under one skip mask, numbered locally from 0 (its root), segment
