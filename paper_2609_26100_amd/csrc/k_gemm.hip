@@ -350,15 +350,21 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   } else if constexpr (EPI == EPI_RESID) {
     // rows whose sequence skips this block keep h, their next-norm input and
     // their partial sums untouched
+    // four adjacent columns per thread: vector loads and stores of h, the
+    // gain and the next-norm input (adjacent in each activation plane)
     const int N = a.N;
-    for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
-      const int row = e / COLS, col = e % COLS;
+    for (int e4 = threadIdx.x; e4 < M * COLS / 4; e4 += blockDim.x) {
+      const int row = e4 / (COLS / 4), col = (e4 % (COLS / 4)) * 4;
       if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
       const size_t idx = (size_t)row * N + n0 + col;
-      const float hn = a.h[idx] + yfin[row * COLS + col];
-      a.h[idx] = hn;
-      store_act<T>(a.xn, a.xn_plane, act_index<T>(row, n0 + col, N), hn * a.g_next[s_seq[row]][n0 + col]);
-      aux[row * COLS + col] = hn * hn;
+      const float4 h0 = *(const float4*)(a.h + idx);
+      const float* y = yfin + row * COLS + col;
+      const float4 hn = make_float4(h0.x + y[0], h0.y + y[1], h0.z + y[2], h0.w + y[3]);
+      *(float4*)(a.h + idx) = hn;
+      const float4 gn = *(const float4*)(a.g_next[s_seq[row]] + n0 + col);
+      store_act4<T>(a.xn, a.xn_plane, act_index<T>(row, n0 + col, N),
+                    make_float4(hn.x * gn.x, hn.y * gn.y, hn.z * gn.z, hn.w * gn.w));
+      *(float4*)(aux + row * COLS + col) = make_float4(hn.x * hn.x, hn.y * hn.y, hn.z * hn.z, hn.w * hn.w);
     }
     __syncthreads();
     // one partial sum of h^2 per 16 columns (the format every norm reads)
@@ -373,11 +379,13 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     static_assert(NT % 2 == 0, "gate and up tiles pair up");
     const int F = a.N >> 1;
     constexpr int PAIRS = NT / 2;
-    for (int e = threadIdx.x; e < M * 16 * PAIRS; e += blockDim.x) {
-      const int row = e / (16 * PAIRS), j = (e / 16) % PAIRS, c = e & 15;
-      const float g = yfin[row * COLS + j * 32 + c];
-      const float u = yfin[row * COLS + j * 32 + 16 + c];
-      store_act<T>(a.act, a.act_plane, act_index<T>(row, (strip * PAIRS + j) * 16 + c, F), silu(g) * u);
+    // four adjacent outputs per thread, one vector store per plane
+    for (int e4 = threadIdx.x; e4 < M * 4 * PAIRS; e4 += blockDim.x) {
+      const int row = e4 / (4 * PAIRS), j = (e4 / 4) % PAIRS, c = (e4 & 3) * 4;
+      const float* g = yfin + row * COLS + j * 32 + c;
+      const float* u = g + 16;
+      store_act4<T>(a.act, a.act_plane, act_index<T>(row, (strip * PAIRS + j) * 16 + c, F),
+                    make_float4(silu(g[0]) * u[0], silu(g[1]) * u[1], silu(g[2]) * u[2], silu(g[3]) * u[3]));
     }
   } else {  // EPI_LOGITS
     const int N = a.N;
