@@ -29,8 +29,9 @@
 //     bf16 mode; fp32 throughout (v_mfma_f32_16x16x4_f32) in the f32 mode.
 // The 8 waves' softmax states meet in LDS (fixed order), tile after tile.
 // With G = 1 the workgroup writes the normalised rows itself.  With G > 1
-// each workgroup writes its partial states, releases them, and bumps a
-// per-(head, sequence) counter; the last to arrive merges the G partials in
+// each workgroup writes its partial states with agent-scope stores, waits
+// for them to land, and bumps a per-(head, sequence) counter; the last to
+// arrive reads them with agent-scope loads and merges the G partials in
 // workgroup order and resets the counter.  No second kernel (a kernel
 // boundary costs about 3 us on this GPU) and bit-reproducible results.
 //
@@ -49,6 +50,17 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ unsigned pack_f16x2(float lo, float hi) {
   const _Float16 a = (_Float16)lo, b = (_Float16)hi;
   return (unsigned)__builtin_bit_cast(unsigned short, a) | ((unsigned)__builtin_bit_cast(unsigned short, b) << 16);
+}
+
+// Partial states travel between workgroups (possibly on different XCDs, whose
+// L2 caches are not coherent with each other) through agent-scope accesses:
+// the stores write through to the level every XCD sees and the loads read
+// from it, so publishing them needs no L2 write-back or invalidation.
+__device__ __forceinline__ void store_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_agent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 #ifndef TSS_ATTN_WAVES
@@ -338,29 +350,35 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
         store_act4<TW>(a.o, a.o_plane, act_index<TW>(row0 + ln, head * HD + dim, a.d),
                        make_float4(num.x / den, num.y / den, num.z / den, num.w / den));
       } else {
-        *(float4*)(po + row * HD + dim) = num;
+        float* dst = po + row * HD + dim;
+        store_agent(dst + 0, num.x);
+        store_agent(dst + 1, num.y);
+        store_agent(dst + 2, num.z);
+        store_agent(dst + 3, num.w);
       }
     }
     if (G > 1 && threadIdx.x < 16) {
-      pm[threadIdx.x * 2 + 0] = sm_mx[threadIdx.x];
-      pm[threadIdx.x * 2 + 1] = sm_den[threadIdx.x];
+      store_agent(pm + threadIdx.x * 2 + 0, sm_mx[threadIdx.x]);
+      store_agent(pm + threadIdx.x * 2 + 1, sm_den[threadIdx.x]);
     }
     __syncthreads();  // the next tile reuses the merge buffers
   }
   if (G == 1) return;
 
-  // Publish this workgroup's partials, then let the last arrival merge.  The
-  // barrier above completed every wave's stores; one thread's device-scope
-  // fence then releases them (and, in the last workgroup, acquires the
-  // others'): on this multi-XCD part a fence writes back / invalidates L2, so
-  // it is issued once per workgroup, not per thread.
+  // Publish this workgroup's partials, then let the last arrival merge.  Each
+  // thread waits until its agent-scope stores are acknowledged (then they are
+  // visible to every XCD), the barrier makes that true of the whole
+  // workgroup, and only then is the arrival counted; the last arrival reads
+  // the partials with agent-scope loads issued after its count returned.
+  // (A device-scope fence instead writes back and invalidates this XCD's
+  // whole L2.)
   __shared__ int last;
   const int ctr = head * gridDim.y + y;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
   if (threadIdx.x == 0) {
-    __threadfence();
-    const int prev = atomicAdd(a.counters + ctr, 1);
+    const int prev = __hip_atomic_fetch_add(a.counters + ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     last = prev == G - 1;
-    if (last) __threadfence();
   }
   __syncthreads();
   if (!last) return;
@@ -389,7 +407,10 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       const float* src = a.part_o + (slot0 * TMAX + t) * 16 * HD + row * HD + dim;
 #pragma unroll
       for (int k = 0; k < kAttnMaxGroups; ++k)
-        if (k < G) v[i][k] = *(const float4*)(src + k * part_stride);
+        if (k < G) {
+          const float* q = src + k * part_stride;
+          v[i][k] = make_float4(load_agent(q), load_agent(q + 1), load_agent(q + 2), load_agent(q + 3));
+        }
     }
   };
   auto merge_round = [&](int base) {
@@ -423,8 +444,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int k = 0; k < kAttnMaxGroups; ++k) {
       if (k < G) {
-        mk[k] = pm[k * TMAX * 32];
-        lk[k] = pm[k * TMAX * 32 + 1];
+        mk[k] = load_agent(pm + k * TMAX * 32);
+        lk[k] = load_agent(pm + k * TMAX * 32 + 1);
       }
     }
     float mx = -1e30f;
