@@ -71,12 +71,12 @@ __device__ __forceinline__ float load_agent(const float* p) {
 #endif
 constexpr int kAttnWaves = TSS_ATTN_WAVES;
 
-// LDS: q tiles [TMAX][64][NQ] uint4 | m, l [W][16] | O [W][64][OS] | mx [16] | f [W][16] | den [16]
+// LDS: q tiles [TMAX][64][NQ] uint4 | m, l [W][16] | O [W][64][OS]
 template <typename TK, int HD, int TMAX>
 constexpr size_t attn_lds() {
   constexpr int NQ = HD / 4 * (int)sizeof(TK) / 16;
   constexpr int OS = HD / 16 * 4 + 1;
-  return (size_t)(TMAX * 64 * NQ * 4 + kAttnWaves * 16 * 2 + kAttnWaves * 64 * OS + 16 + kAttnWaves * 16 + 16) * 4;
+  return (size_t)(TMAX * 64 * NQ * 4 + kAttnWaves * 16 * 2 + kAttnWaves * 64 * OS) * 4;
 }
 
 // TK = KV element type (_Float16 or float); TW = weight type of the mode
@@ -289,13 +289,25 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   }
 
   // Merge the waves' states tile by tile: O = sum_w f_w O_w / sum_w f_w l_w
-  // with f_w = 2^(m_w - max_w m_w), summed in wave order.
+  // with f_w = 2^(m_w - max_w m_w), summed in wave order.  Every thread
+  // derives the weights of the row it writes from the waves' (m, l) in LDS
+  // (the same operations in the same order everywhere), so one barrier
+  // separates the waves' writes from the combination.
   float* sm_m = smem + TMAX * 64 * NQ * 4;  // [W][16], after the q tiles
   float* sm_l = sm_m + W * 16;              // [W][16]
   float* sm_o = sm_l + W * 16;              // [W][64][OS]
-  float* sm_mx = sm_o + W * 64 * OS;        // [16]
-  float* sm_f = sm_mx + 16;                 // [W][16]
-  float* sm_den = sm_f + W * 16;            // [16]
+  auto row_weights = [&](int row, float (&f)[W]) {
+    float mx = -1e30f;
+#pragma unroll
+    for (int w = 0; w < W; ++w) mx = fmaxf(mx, sm_m[w * 16 + row]);
+    float den = 0.f;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      f[w] = exp2f(sm_m[w * 16 + row] - mx);
+      den += f[w] * sm_l[w * 16 + row];
+    }
+    return make_float2(mx, den);
+  };
   const size_t slot = ((size_t)head * gridDim.y + y) * a.groups + g;  // this workgroup's partial slot
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) {
@@ -309,20 +321,6 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) sm_o[(wave * 64 + lane) * OS + n * 4 + v] = O[t][n][v];
     __syncthreads();
-    if (threadIdx.x < 16) {
-      float mx = -1e30f;
-      for (int w = 0; w < W; ++w) mx = fmaxf(mx, sm_m[w * 16 + threadIdx.x]);
-      sm_mx[threadIdx.x] = mx;
-    }
-    __syncthreads();
-    if (threadIdx.x < W * 16) sm_f[threadIdx.x] = exp2f(sm_m[threadIdx.x] - sm_mx[threadIdx.x & 15]);
-    __syncthreads();
-    if (threadIdx.x < 16) {
-      float den = 0.f;
-      for (int w = 0; w < W; ++w) den += sm_f[w * 16 + threadIdx.x] * sm_l[w * 16 + threadIdx.x];
-      sm_den[threadIdx.x] = den;
-    }
-    __syncthreads();
 
     // Output (source lane src, row v of its four, tiles n0 .. n0+3): node row
     // 4*(src/16)+v of the tile, dims NO*(src%16)+n0 .. +3 (contiguous, so one
@@ -335,18 +333,20 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       const int row = (src >> 4) * 4 + v;
       const int ln = t * 16 + row;
       if (ln >= Ms) continue;
+      float f[W];
+      const float2 md = row_weights(row, f);
       float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
       for (int w = 0; w < W; ++w) {
-        const float f = sm_f[w * 16 + row];
         const float* so = sm_o + (w * 64 + src) * OS + n0 * 4 + v;
-        num.x += f * so[0];
-        num.y += f * so[4];
-        num.z += f * so[8];
-        num.w += f * so[12];
+        num.x += f[w] * so[0];
+        num.y += f[w] * so[4];
+        num.z += f[w] * so[8];
+        num.w += f[w] * so[12];
       }
       const int dim = NO * (src & 15) + n0;
       if (G == 1) {
-        const float den = sm_den[row];
+        const float den = md.y;
         store_act4<TW>(a.o, a.o_plane, act_index<TW>(row0 + ln, head * HD + dim, a.d),
                        make_float4(num.x / den, num.y / den, num.z / den, num.w / den));
       } else {
@@ -358,8 +358,10 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       }
     }
     if (G > 1 && threadIdx.x < 16) {
-      store_agent(pm + threadIdx.x * 2 + 0, sm_mx[threadIdx.x]);
-      store_agent(pm + threadIdx.x * 2 + 1, sm_den[threadIdx.x]);
+      float f[W];
+      const float2 md = row_weights(threadIdx.x, f);
+      store_agent(pm + threadIdx.x * 2 + 0, md.x);
+      store_agent(pm + threadIdx.x * 2 + 1, md.y);
     }
     __syncthreads();  // the next tile reuses the merge buffers
   }

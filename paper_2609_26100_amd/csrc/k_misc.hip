@@ -9,73 +9,76 @@ namespace tss {
 // gain of the first RMSNorm the row's sequence meets; ss_out[m][p] = sum of
 // h[m][k]^2 over the 16 columns of part p (the format every projection
 // epilogue writes, so each norm reads d/16 parts whatever produced them).
-// Each thread gathers up to four 16-byte chunks of the row, issued together.
 // The step's parameters arrive by value and workgroup 0 stores them for the
 // later kernels of the step (this replaces a separate host-to-device copy,
 // which costs as much as a kernel launch).
 template <typename T>
 __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
-  constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte chunk
-  constexpr int MAXC = 4;                 // chunks per thread (d <= 4 * 256 * E)
-  __shared__ float rowv[4 * 256 * 8];
+  constexpr int E = 16 / (int)sizeof(T);  // elements of T per 16-byte chunk
   const int m = blockIdx.x;
-  const int d = a.d, nch = d / E;
+  const int d = a.d;
   if (m == 0) {
     const uint32_t* src = (const uint32_t*)&a.sp;
     uint32_t* dst = (uint32_t*)a.sp_dev;
     for (int i = threadIdx.x; i < (int)(sizeof(StepParams) / 4); i += 256) dst[i] = src[i];
   }
   const float* gain = a.gain[a.sp.row_seq[m]];
-  if (a.src_h) {
-    // resume from a saved residual row (fp32, 16 bytes per chunk)
-    const float4* src = (const float4*)(a.src_h + (size_t)(m - a.sp.seq_row0[a.sp.row_seq[m]]) * d);
-    for (int c = threadIdx.x; c < d / 4; c += 256) {
-      const float4 v4 = src[c];
-      const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+  // Each thread takes whole 16-column parts (up to two; d <= 8192): the
+  // row's chunks and the gains of its parts are requested together, and the
+  // part's sum of squares needs no exchange between threads.  The row is the
+  // token's embedding (T) or a saved residual row (fp32).
+  const bool resume = a.src_h != nullptr;
+  const int CPP = resume ? 4 : 16 / E;  // 16-byte chunks per part
+  const uint4* row = resume ? (const uint4*)(a.src_h + (size_t)(m - a.sp.seq_row0[a.sp.row_seq[m]]) * d)
+                            : (const uint4*)((const T*)a.embed + (size_t)a.sp.tok[m] * d);
+  const int nparts = d / 16;
+  uint4 raw[2][4];
+  float4 gv[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int p = threadIdx.x + 256 * i;
+    if (p >= nparts) break;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j < CPP) raw[i][j] = row[p * CPP + j];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) gv[i][q] = ((const float4*)gain)[p * 4 + q];
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int p = threadIdx.x + 256 * i;
+    if (p >= nparts) break;
+    float v[16];
+    if (resume) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int k = c * 4 + j;
-        a.h[(size_t)m * d + k] = vv[j];
-        store_act<T>(a.xn, a.xn_plane, act_index<T>(m, k, d), vv[j] * gain[k]);
-        rowv[k] = vv[j];
+        const float4 f = __builtin_bit_cast(float4, raw[i][j]);
+        v[4 * j] = f.x;
+        v[4 * j + 1] = f.y;
+        v[4 * j + 2] = f.z;
+        v[4 * j + 3] = f.w;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 16 / E; ++j) {
+        const T* e = (const T*)&raw[i][j];
+#pragma unroll
+        for (int k = 0; k < E; ++k) v[j * E + k] = (float)e[k];
       }
     }
-    __syncthreads();
-    for (int p = threadIdx.x; p < d / 16; p += 256) {
-      float s = 0.f;
+    float ss = 0.f;
 #pragma unroll
-      for (int k = 0; k < 16; ++k) s += rowv[p * 16 + k] * rowv[p * 16 + k];
-      a.ss_out[(size_t)m * a.ss_stride + p] = s;
+    for (int k = 0; k < 16; ++k) ss += v[k] * v[k];
+    float* hrow = a.h + (size_t)m * d + p * 16;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 h4 = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+      *(float4*)(hrow + 4 * q) = h4;
+      const float4 g4 = gv[i][q];
+      store_act4<T>(a.xn, a.xn_plane, act_index<T>(m, p * 16 + 4 * q, d),
+                    make_float4(h4.x * g4.x, h4.y * g4.y, h4.z * g4.z, h4.w * g4.w));
     }
-    return;
-  }
-  const T* row = (const T*)a.embed + (size_t)a.sp.tok[m] * d;
-  uint4 raw[MAXC];
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = threadIdx.x + i * 256;
-    raw[i] = c < nch ? ((const uint4*)row)[c] : uint4{0, 0, 0, 0};
-  }
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = threadIdx.x + i * 256;
-    if (c >= nch) break;
-    const T* e = (const T*)&raw[i];
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-      const int k = c * E + j;
-      const float v = (float)e[j];
-      a.h[(size_t)m * d + k] = v;
-      store_act<T>(a.xn, a.xn_plane, act_index<T>(m, k, d), v * gain[k]);
-      rowv[k] = v;
-    }
-  }
-  __syncthreads();
-  for (int p = threadIdx.x; p < d / 16; p += 256) {
-    float s = 0.f;
-#pragma unroll
-    for (int k = 0; k < 16; ++k) s += rowv[p * 16 + k] * rowv[p * 16 + k];
-    a.ss_out[(size_t)m * a.ss_stride + p] = s;
+    a.ss_out[(size_t)m * a.ss_stride + p] = ss;
   }
 }
 

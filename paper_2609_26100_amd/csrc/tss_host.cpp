@@ -81,7 +81,7 @@ int cfg_ok(const tss_model_cfg* c) {
   if (c->dtype != TSS_F32 && c->dtype != TSS_BF16) return 0;
   if (c->max_nodes < 1 || c->max_nodes > kMaxNodes) return 0;
   if (c->max_batch < 1 || c->max_batch > kMaxBatch) return 0;
-  if (c->dtype == TSS_F32 && c->d_model > 4096) return 0;  // embedding gather: 4 chunks of 4 per thread
+  if (c->dtype == TSS_F32 && c->d_model > 4096) return 0;  // the fp32 mode serves small models; validated up to 4096
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return 0;
   return 1;
 }

@@ -69,7 +69,7 @@ def test_cfg_batch_capacity():
     big = abi.make_cfg(synth.LLAMA_13B, max_nodes=64, max_batch=8)   # capped at 128 rows
     assert abi.tss_workspace_bytes(big) < 2 * abi.tss_workspace_bytes(abi.make_cfg(synth.LLAMA_13B, 64, 2))
     wide = abi.make_cfg(synth.TINY)
-    wide.d_model, wide.n_heads = 8192, 128     # fp32 embedding gather covers d <= 4096
+    wide.d_model, wide.n_heads = 8192, 128     # the fp32 mode takes d <= 4096
     assert abi.tss_cfg_check(wide) == abi.TSS_EINVAL
 
 
