@@ -55,12 +55,22 @@ __device__ __forceinline__ unsigned pack_f16x2(float lo, float hi) {
 // Partial states travel between workgroups (possibly on different XCDs, whose
 // L2 caches are not coherent with each other) through agent-scope accesses:
 // the stores write through to the level every XCD sees and the loads read
-// from it, so publishing them needs no L2 write-back or invalidation.
+// from it (scope bit sc1), so publishing them needs no L2 write-back or
+// invalidation.  The partial outputs go through a buffer resource (one
+// 16-byte access per four floats); offsets are in bytes.
+constexpr int kScopeAgent = 16;  // cache-policy operand of buffer accesses: sc1
 __device__ __forceinline__ void store_agent(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ float load_agent(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_agent4(__amdgpu_buffer_rsrc_t r, int off, float4 v) {
+  typedef float f4v __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(f4v, v), r, off, 0, kScopeAgent);
+}
+__device__ __forceinline__ float4 load_agent4(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kScopeAgent));
 }
 
 #ifndef TSS_ATTN_WAVES
@@ -309,6 +319,9 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     return make_float2(mx, den);
   };
   const size_t slot = ((size_t)head * gridDim.y + y) * a.groups + g;  // this workgroup's partial slot
+  // the partial outputs of the launch: [heads * items * groups][TMAX][16][HD] floats
+  const __amdgpu_buffer_rsrc_t pres = __builtin_amdgcn_make_buffer_rsrc(
+      a.part_o, (short)0, (int)((size_t)a.n_heads * gridDim.y * a.groups * TMAX * 16 * HD * sizeof(float)), 0x00020000);
 #pragma unroll
   for (int t = 0; t < TMAX; ++t) {
     if (t >= T) break;
@@ -327,7 +340,6 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     // vector store each); value sum_w f_w O_w (unnormalised), in wave order.
     static_assert(NO % 4 == 0, "four output tiles per store");
     float* pm = a.part_ml + (slot * TMAX + t) * 32;      // [16][2]
-    float* po = a.part_o + (slot * TMAX + t) * 16 * HD;  // [16][HD]
     for (int e = threadIdx.x; e < 64 * NO; e += blockDim.x) {
       const int src = e / NO, v = (e / (NO / 4)) % 4, n0 = (e % (NO / 4)) * 4;
       const int row = (src >> 4) * 4 + v;
@@ -350,11 +362,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
         store_act4<TW>(a.o, a.o_plane, act_index<TW>(row0 + ln, head * HD + dim, a.d),
                        make_float4(num.x / den, num.y / den, num.z / den, num.w / den));
       } else {
-        float* dst = po + row * HD + dim;
-        store_agent(dst + 0, num.x);
-        store_agent(dst + 1, num.y);
-        store_agent(dst + 2, num.z);
-        store_agent(dst + 3, num.w);
+        store_agent4(pres, (int)(((slot * TMAX + t) * 16 * HD + row * HD + dim) * sizeof(float)), num);
       }
     }
     if (G > 1 && threadIdx.x < 16) {
@@ -406,13 +414,10 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       const int e4 = min(base + i * (int)blockDim.x + (int)threadIdx.x, n_e4 - 1);
       const int e = e4 * 4;
       const int t = e / (16 * HD), row = (e / HD) % 16, dim = e % HD;
-      const float* src = a.part_o + (slot0 * TMAX + t) * 16 * HD + row * HD + dim;
+      const size_t src = (slot0 * TMAX + t) * 16 * HD + row * HD + dim;  // floats
 #pragma unroll
       for (int k = 0; k < kAttnMaxGroups; ++k)
-        if (k < G) {
-          const float* q = src + k * part_stride;
-          v[i][k] = make_float4(load_agent(q), load_agent(q + 1), load_agent(q + 2), load_agent(q + 3));
-        }
+        if (k < G) v[i][k] = load_agent4(pres, (int)((src + k * part_stride) * sizeof(float)));
     }
   };
   auto merge_round = [&](int base) {
