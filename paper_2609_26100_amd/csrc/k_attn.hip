@@ -36,9 +36,9 @@
 // boundary costs about 3 us on this GPU) and bit-reproducible results.
 //
 // An item's G (at most `groups`, at least one page per wave, at most
-// pages / (4 T)) is derived on the device from its context length, so launch
-// arguments do not depend on context lengths; workgroups beyond an item's G
-// exit at once.
+// pages / (4 T), and in a batch of sequences one per `pages_per_wg` pages) is
+// derived on the device from its context length, so launch arguments do not
+// depend on context lengths; workgroups beyond an item's G exit at once.
 #include "tss_internal.h"
 
 namespace tss {
@@ -150,7 +150,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   const int n_pages = (n_kv + a.item_slots[y] + kPage - 1) / kPage;
   // workgroups of this item: at most groups, at least a page per wave, and
   // few enough that partial states (T tiles each) stay well below the pages
-  const int G = max(1, min(a.groups, min((n_pages + W - 1) / W, n_pages / (TSS_ATTN_PART_DIV * T))));
+  const int cap = a.pages_per_wg > 0 ? min(a.groups, (n_pages + a.pages_per_wg - 1) / a.pages_per_wg) : a.groups;
+  const int G = max(1, min(cap, min((n_pages + W - 1) / W, n_pages / (TSS_ATTN_PART_DIV * T))));
   if (g >= G) {                                      // uniform over the workgroup
     __builtin_amdgcn_s_waitcnt(0);                   // let the early page load land first
     return;

@@ -63,11 +63,21 @@ int row_cap(const tss_model_cfg* c) {
 int attn_groups(int n_heads, int n_items) {
   return std::max(1, std::min(kAttnMaxGroups, kAttnTargetWGs / (n_heads * n_items)));
 }
+// Workgroups per (head, item) of a launch whose items come from n_items
+// different KV sequences (pages_per_seq pages each at most): one per
+// kAttnPagesPerWG pages of the longest possible context, within
+// kAttnBatchSlots partial-state slots.
+int attn_batch_groups(int n_heads, int n_items, int pages_per_seq) {
+  const int by_pages = (pages_per_seq + kAttnPagesPerWG - 1) / kAttnPagesPerWG;
+  return std::max(1, std::min(kAttnMaxGroups, std::min(by_pages, kAttnBatchSlots / (n_heads * n_items))));
+}
 // partial-state slots of one attention launch: n_heads * n_items * groups
-// over every item count (at most max(kAttnTargetWGs, n_heads * n_items))
+// over every item count (at most max(kAttnTargetWGs, n_heads * n_items)),
+// and up to kAttnBatchSlots when the context serves batches of sequences
 size_t attn_slots(const tss_model_cfg* c) {
   size_t m = 0;
   for (int n = 1; n <= kAttnMaxItems; ++n) m = std::max(m, (size_t)c->n_heads * n * attn_groups(c->n_heads, n));
+  if (c->max_batch > 1) m = std::max(m, (size_t)kAttnBatchSlots);
   return m;
 }
 
@@ -804,7 +814,13 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
       a.part_o = (float*)(ws + c->wsl.part_o);
       a.part_ml = (float*)(ws + c->wsl.part_ml);
       a.counters = (int*)(ws + c->wsl.counters);
-      a.groups = attn_groups(H, n_act);
+      if (!one_seq && n_act > 1) {
+        a.groups = attn_batch_groups(H, n_act, pps);
+        a.pages_per_wg = kAttnPagesPerWG;
+      } else {
+        a.groups = attn_groups(H, n_act);
+        a.pages_per_wg = 0;
+      }
       a.layer = l;
       a.n_pages_pool = c->kvl.n_pages;
       a.n_heads = H;

@@ -53,13 +53,21 @@ constexpr int kTileBytes = 1024;   // one packed 16 x KC weight tile
 constexpr int kAttnMaxGroups = 16; // workgroups per (head, sequence) in attention
 constexpr int kAttnMaxTiles = 4;   // 16-row tiles of one attention item (64 rows)
 constexpr int kAttnMaxItems = 16;  // attention items (row ranges of one KV sequence) of one launch
-// attention workgroups one launch aims for: one round, a little under one
-// per CU (measured best on the 7B, 13B and 33B shapes)
+// attention workgroups one launch of a single sequence aims for: one per CU
+// (with cross-workgroup merges through agent-scope accesses, 256 beats the
+// 208 that was best while each merge needed device-scope fences: 7B chain
+// step 3051 -> 3038 us, 60-node tree 5256 -> 5248 us)
 #ifndef TSS_ATTN_TARGET_WGS
-#define TSS_ATTN_TARGET_WGS 208
+#define TSS_ATTN_TARGET_WGS 256
 #endif
 constexpr int kAttnTargetWGs = TSS_ATTN_TARGET_WGS;
 constexpr int kArgPages = 256;     // page ids passed in kernel arguments (one sequence, up to 4096 tokens)
+// attention over several KV sequences (a batch): an item takes one workgroup
+// per kAttnPagesPerWG pages of its sequence (8 per wave), so a long context
+// is walked by several workgroups instead of bounding the launch; all the
+// launch's partial-state slots stay within kAttnBatchSlots
+constexpr int kAttnPagesPerWG = 64;
+constexpr int kAttnBatchSlots = 2048;
 
 template <typename T> struct Mode;
 template <> struct Mode<__bf16> {
@@ -207,6 +215,7 @@ struct AttnArgs {
   float* part_ml;          // [slots][kAttnMaxTiles][16][2] (max in log2 units, sum)
   int* counters;           // [H * kAttnMaxItems] arrivals, zero between launches
   int groups;              // most workgroups per (head, item)
+  int pages_per_wg;        // > 0: an item takes ceil(pages / pages_per_wg) workgroups (at most groups)
   int layer, n_pages_pool, n_heads, d;
   float scale_log2;        // log2(e) / sqrt(hd)
   // per item, 32-bit so that the kernel reads them with scalar loads
