@@ -118,8 +118,15 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   const int waves = blockDim.x >> 6;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r16 = lane & 15, grp = lane >> 4;
-  const int strip = blockIdx.x;
   const int M = a.M, K = a.K, nkc = a.nkc;
+  // strip and, with a K split, this workgroup's chunks [c_lo, c_hi) of K
+  // (only the residual projections with 2+ row tiles split K: every other
+  // instantiation compiles with ks = 1)
+  constexpr bool SPLIT = EPI == EPI_RESID && MT >= 2;
+  const int ks = SPLIT ? a.ksplit : 1;
+  const int strip = SPLIT ? (int)blockIdx.x / ks : (int)blockIdx.x;
+  const int split = SPLIT ? (int)blockIdx.x - strip * ks : 0;
+  const int c_lo = SPLIT ? split * nkc / ks : 0, c_hi = SPLIT ? (split + 1) * nkc / ks : nkc;
   // weight tile nt of this strip, chunk c, at wb[nt] + c * wstep: plain
   // matrices store a 16-row tile's chunks consecutively; gate and up tiles of
   // one pair alternate chunk by chunk
@@ -182,7 +189,8 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   // products land in output rows that are never stored) and the main loop
   // only runs while every refill is in range; the last chunks are finished
   // by a short tail.
-  const int n_my = wave < nkc ? (nkc - wave + waves - 1) / waves : 0;
+  const int nkc_s = c_hi - c_lo;
+  const int n_my = wave < nkc_s ? (nkc_s - wave + waves - 1) / waves : 0;
   uint4 wv[D][NT];
   uint4 xv[D][MT][S];
   // Activation tiles through a buffer resource: a padded row (>= M) gets an
@@ -197,7 +205,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     xoff[mt] = mt * 16 + r16 < M ? (mt * nkc * 64 + lane) * 16 : kPastEnd;
   const int plane_bytes = (int)(a.x_plane * sizeof(T));
   auto issue = [&](uint4 (&w)[NT], uint4 (&xs)[MT][S], int i) {
-    const int c = wave + i * waves;
+    const int c = c_lo + wave + i * waves;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) w[nt] = load_stream(wb[nt] + (size_t)c * wstep);
 #pragma unroll
@@ -280,6 +288,44 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * RC + col];
       yfin[row * COLS + c0 + col] = s;
     }
+  }
+
+  if (SPLIT && ks > 1) {
+    // K split: publish this workgroup's sums (agent-scope stores: visible to
+    // every XCD once acknowledged), count the arrival, and let the last
+    // workgroup of the strip add the ks partial products in split order
+    __shared__ int s_last;
+    __syncthreads();  // yfin complete
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    const size_t slot_floats = (size_t)a.Mp * COLS;
+    const __amdgpu_buffer_rsrc_t pres = __builtin_amdgcn_make_buffer_rsrc(
+        a.kpart, (short)0, (int)(gridDim.x * slot_floats * sizeof(float)), 0x00020000);
+    constexpr int kScopeAgent = 16;  // cache-policy operand: sc1 (agent scope)
+    for (int e4 = threadIdx.x; e4 < M * COLS / 4; e4 += blockDim.x)
+      __builtin_amdgcn_raw_buffer_store_b128(*(const f4v*)(yfin + 4 * e4), pres,
+                                             (int)((blockIdx.x * slot_floats + 4 * e4) * sizeof(float)), 0,
+                                             kScopeAgent);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0)
+      s_last = __hip_atomic_fetch_add(a.kcount + strip, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ks - 1;
+    __syncthreads();
+    if (!s_last) return;
+    for (int e4 = threadIdx.x; e4 < M * COLS / 4; e4 += blockDim.x) {
+      f4v v[kMaxKSplit];
+#pragma unroll
+      for (int k = 0; k < kMaxKSplit; ++k)
+        if (k < ks && k != split)
+          v[k] = __builtin_amdgcn_raw_buffer_load_b128(
+              pres, (int)(((size_t)(strip * ks + k) * slot_floats + 4 * e4) * sizeof(float)), 0, kScopeAgent);
+      const f4v own = *(const f4v*)(yfin + 4 * e4);
+      f4v t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < kMaxKSplit; ++k)
+        if (k < ks) t += k == split ? own : v[k];
+      *(f4v*)(yfin + 4 * e4) = t;
+    }
+    if (threadIdx.x == 0) a.kcount[strip] = 0;
   }
 
   if (!ss_early) {
@@ -466,10 +512,11 @@ static hipError_t launch_v(const GemmArgs& a, hipStream_t s) {
   // LDS: up to 64 rows the cross-wave reduction stays within 64 KiB
   // (4-tile blocks and more than 4 row tiles may use most of the CU's LDS)
   const size_t cap = gemm_lds_cap<MT, NT>();
-  int waves = a.nkc < 8 ? a.nkc : 8;
+  const int nkc_min = a.nkc / a.ksplit;  // chunks of the smallest K split
+  int waves = nkc_min < 8 ? nkc_min : 8;
   while (waves > 1 && gemm_lds<MT, NT>(waves) > cap) waves >>= 1;
   const size_t lds = gemm_lds<MT, NT>(waves);
-  dim3 grid(a.N / (16 * NT)), block(waves * 64);
+  dim3 grid(a.N / (16 * NT) * a.ksplit), block(waves * 64);
   TSS_LAUNCH((k_gemm<T, MT, NT, EPI>), grid, block, lds, s, a);
   return hipGetLastError();
 }
@@ -508,6 +555,8 @@ static hipError_t launch_rows(int epi, int nt, const GemmArgs& a, hipStream_t s)
 
 hipError_t launch_gemm(bool bf16, int epi, int mt, int nt, const GemmArgs& a, hipStream_t s) {
   if (nt != gemm_tiles(epi, mt, a.N)) return hipErrorInvalidValue;
+  if (a.ksplit != gemm_ksplit(epi, mt, a.N, a.nkc) || (a.ksplit > 1 && (!a.kpart || !a.kcount)))
+    return hipErrorInvalidValue;
   if (bf16) {
     switch (mt) {
       case 1: return launch_rows<__bf16, 1>(epi, nt, a, s);

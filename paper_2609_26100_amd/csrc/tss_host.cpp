@@ -43,8 +43,8 @@ struct WeightLayout {
 };
 
 struct WsLayout {
-  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, counters, logits, am_val, am_idx, greedy,
-      total;
+  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, counters, kpart, kcount, logits, am_val,
+      am_idx, greedy, total;
 };
 
 // weight element bytes; the KV cache uses the same width (fp16 in the bf16
@@ -138,6 +138,8 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   w.part_o = take(slots * kAttnMaxTiles * 16 * c->head_dim * 4);
   w.part_ml = take(slots * kAttnMaxTiles * 16 * 2 * 4);
   w.counters = take((size_t)c->n_heads * kAttnMaxItems * 4);
+  w.kpart = take((size_t)kMaxKSplit * d * Mp * 4);  // K-split partial products of the residual projections
+  w.kcount = take((d / 16) * 4);
   w.logits = take(Mp * v * 4);
   w.am_val = take((v / 16) * Mp * 4);
   w.am_idx = take((v / 16) * Mp * 4);
@@ -399,6 +401,8 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
   if (e == hipSuccess)
     step("attention counters",
          hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * kAttnMaxItems * 4, c->stream));
+  if (e == hipSuccess)
+    step("K-split counters", hipMemsetAsync(c->ws + c->wsl.kcount, 0, (size_t)(cfg->d_model / 16) * 4, c->stream));
   if (e == hipSuccess) step("stream sync", hipStreamSynchronize(c->stream));
   if (e == hipSuccess) step("attention LDS attribute", init_kernel_attributes());
   if (e == hipSuccess) step("projection LDS attribute", init_gemm_attributes());
@@ -732,6 +736,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
   base.ss_stride = d / 16;
   base.ss_nparts = d / 16;
   base.am_stride = cf.vocab / 16;
+  base.ksplit = 1;
   base.sp = sp_dev;
   base.row_on[0] = base.row_on[1] = ~0ull;
 
@@ -844,6 +849,9 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
       for (int i = 0; i < kMaxSegs; ++i) a.g_next[i] = (const float*)(c->w + W.mlp_norm);
       a.ss_out = (float*)(ws + c->wsl.ss_m);
       ProfScope ps(c, TSS_K_OPROJ, l);
+      a.ksplit = gemm_ksplit(EPI_RESID, mt, a.N, a.nkc);
+      a.kpart = (float*)(ws + c->wsl.kpart);
+      a.kcount = (int*)(ws + c->wsl.kcount);
       HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, gemm_tiles(EPI_RESID, mt, a.N), a, s), "o gemm");
       ps.done();
     }
@@ -876,6 +884,9 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
       for (int i = 0; i < kMaxSegs; ++i) a.g_next[i] = attn_gain_of(c, i < B ? next_active(c, i, l) : L);
       a.ss_out = (float*)(ws + c->wsl.ss_a);
       ProfScope ps(c, TSS_K_DOWN, l);
+      a.ksplit = gemm_ksplit(EPI_RESID, mt, a.N, a.nkc);
+      a.kpart = (float*)(ws + c->wsl.kpart);
+      a.kcount = (int*)(ws + c->wsl.kcount);
       HIPCHK(launch_gemm(c->bf16, EPI_RESID, mt, gemm_tiles(EPI_RESID, mt, a.N), a, s), "down gemm");
       ps.done();
     }

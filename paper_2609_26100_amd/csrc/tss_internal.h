@@ -67,6 +67,9 @@ constexpr int kArgPages = 256;     // page ids passed in kernel arguments (one s
 // is walked by several workgroups instead of bounding the launch; all the
 // launch's partial-state slots stay within kAttnBatchSlots
 constexpr int kAttnPagesPerWG = 64;
+// most K splits of one projection launch (the residual projections with
+// more than one row tile, see gemm_ksplit)
+constexpr int kMaxKSplit = 4;
 constexpr int kAttnBatchSlots = 2048;
 
 template <typename T> struct Mode;
@@ -170,6 +173,12 @@ struct GemmArgs {
   int norm_dim;
   float eps;
   int Mp;                  // row stride of the partial-sum arrays
+  // K split (> 1): workgroup blockIdx.x takes strip blockIdx.x / ksplit over
+  // its share of K; the ksplit partial products of a strip meet in kpart
+  // (agent-scope accesses) and the last workgroup to arrive finishes the strip
+  int ksplit;
+  float* kpart;            // [strips * ksplit][Mp][16 * NT] partial products
+  int* kcount;             // [strips] arrivals, zero between launches
   const StepParams* sp;
   // rows whose segment runs this block (bit r of row_on[r / 64]); the QKV
   // and residual epilogues write nothing for the other rows
@@ -312,11 +321,14 @@ hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base,
 // 3133 -> 3096 us, the 60-node tree 5903 -> 5792 us); with 2-4 row tiles
 // gate/up takes 8 tiles when they fit 256 workgroups (the 60-node tree
 // 5851 -> 5531 us; with 5 row tiles they spill and the 13B batch slows).
-// (Splitting K over
-// workgroups to widen the blocks
-// further measured slower: partial sums and a device-scope fence per
-// workgroup.)
+// The residual projections with 2-7 row tiles take four-tile blocks over a
+// share of K instead (gemm_ksplit; the partial tiles meet through agent-scope
+// accesses, with no device-scope fence).
 inline int gemm_tiles(int epi, int mt, int N) {
+  // residual projections with 2-7 row tiles: four-tile blocks over a share of
+  // K (gemm_ksplit), so each workgroup re-reads a quarter of the activation
+  // tiles that a one-tile block over all of K would
+  if (epi == EPI_RESID && mt >= 2 && mt <= 7 && N % 64 == 0) return 4;
   // gate/up with 2-4 row tiles: eight-tile blocks (four pairs) when they fit
   // one round (7B: 172 workgroups instead of 344 in 1.34 rounds; more row
   // tiles would spill)
@@ -336,6 +348,18 @@ inline int gemm_tiles(int epi, int mt, int N) {
   for (int nt = 1; nt <= 4; nt *= 2)
     if (N % (16 * nt) == 0 && N / (16 * nt) <= 256) return nt;
   return N % 64 == 0 ? 4 : (N % 32 == 0 ? 2 : 1);
+}
+
+// K splits of a projection launch: the residual projections with 2-7 row
+// tiles split K so that their four-tile blocks still fill about one round of
+// 256 workgroups (7B: 64 strips x 4, 13B: 80 x 3, 33B: 104 x 2), each split
+// keeping at least one chunk per wave.  nkc = K chunks of the matrix.
+inline int gemm_ksplit(int epi, int mt, int N, int nkc) {
+  if (!(epi == EPI_RESID && mt >= 2 && mt <= 7 && N % 64 == 0)) return 1;
+  int ks = 256 / (N / 64);
+  ks = ks < 1 ? 1 : (ks > kMaxKSplit ? kMaxKSplit : ks);
+  while (ks > 1 && nkc / ks < 8) --ks;
+  return ks;
 }
 
 }  // namespace tss
