@@ -321,14 +321,17 @@ hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base,
 // 3133 -> 3096 us, the 60-node tree 5903 -> 5792 us); with 2-4 row tiles
 // gate/up takes 8 tiles when they fit 256 workgroups (the 60-node tree
 // 5851 -> 5531 us; with 5 row tiles they spill and the 13B batch slows).
-// The residual projections with 2-7 row tiles take four-tile blocks over a
-// share of K instead (gemm_ksplit; the partial tiles meet through agent-scope
+// The residual projections with 2-8 row tiles take four- (two-) tile blocks
+// over a share of K instead (gemm_ksplit; the partial tiles meet through agent-scope
 // accesses, with no device-scope fence).
 inline int gemm_tiles(int epi, int mt, int N) {
   // residual projections with 2-7 row tiles: four-tile blocks over a share of
   // K (gemm_ksplit), so each workgroup re-reads a quarter of the activation
   // tiles that a one-tile block over all of K would
   if (epi == EPI_RESID && mt >= 2 && mt <= 7 && N % 64 == 0) return 4;
+  // eight row tiles: two-tile blocks (four would spill), split where that
+  // fills the round (7B: 128 strips x 2; 7B 64-mask sweep 16.05 -> 14.97 ms)
+  if (epi == EPI_RESID && mt == 8 && N % 32 == 0 && N / 32 <= 256) return 2;
   // gate/up with 2-4 row tiles: eight-tile blocks (four pairs) when they fit
   // one round (7B: 172 workgroups instead of 344 in 1.34 rounds; more row
   // tiles would spill)
@@ -352,11 +355,14 @@ inline int gemm_tiles(int epi, int mt, int N) {
 
 // K splits of a projection launch: the residual projections with 2-7 row
 // tiles split K so that their four-tile blocks still fill about one round of
-// 256 workgroups (7B: 64 strips x 4, 13B: 80 x 3, 33B: 104 x 2), each split
-// keeping at least one chunk per wave.  nkc = K chunks of the matrix.
+// 256 workgroups (7B: 64 strips x 4, 13B: 80 x 3, 33B: 104 x 2), and with 8
+// row tiles their two-tile blocks (7B: 128 x 2), each split keeping at least
+// one chunk per wave.  nkc = K chunks of the matrix.
 inline int gemm_ksplit(int epi, int mt, int N, int nkc) {
-  if (!(epi == EPI_RESID && mt >= 2 && mt <= 7 && N % 64 == 0)) return 1;
-  int ks = 256 / (N / 64);
+  const bool four = epi == EPI_RESID && mt >= 2 && mt <= 7 && N % 64 == 0;
+  const bool two = epi == EPI_RESID && mt == 8 && N % 32 == 0 && N / 32 <= 256;
+  if (!four && !two) return 1;
+  int ks = 256 / (N / (four ? 64 : 32));
   ks = ks < 1 ? 1 : (ks > kMaxKSplit ? kMaxKSplit : ks);
   while (ks > 1 && nkc / ks < 8) --ks;
   return ks;
