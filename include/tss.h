@@ -115,17 +115,25 @@ typedef struct {
   int32_t max_batch;   /* most sequences of one tss_verify_batch (1 for single-sequence use) */
 } tss_model_cfg;
 
-/* Checks the constraints above.  Pure host function.  TSS_OK or TSS_EINVAL. */
+/* Checks the constraints above.  Pure host function.  TSS_OK or TSS_EINVAL.
+ * Paper: Appendix / Models (the LLaMA target shapes the step serves). */
 int tss_cfg_check(const tss_model_cfg* cfg);
 
-/* Size queries (bytes); 0 when cfg is invalid. */
+/* Size queries (bytes); 0 when cfg is invalid.  The caller allocates these
+ * device buffers (the library allocates none).  Paper: Appendix / Models
+ * (weights), Problem Formulation (the workspace of one parallel verification
+ * pass), Experiments / Models (the KV cache the underlying method keeps). */
 size_t tss_weights_bytes(const tss_model_cfg* cfg);
 size_t tss_workspace_bytes(const tss_model_cfg* cfg);
 size_t tss_kv_bytes(const tss_model_cfg* cfg, int32_t n_seqs, int32_t max_tokens_per_seq);
 
 /* Creates a context bound to hip_stream (a hipStream_t; NULL = the null
  * stream), a packed-weight buffer of tss_weights_bytes() and a workspace of
- * tss_workspace_bytes(), both device memory owned by the caller. */
+ * tss_workspace_bytes(), both device memory owned by the caller, who keeps
+ * them alive until tss_destroy.  *out receives the context (NULL on failure).
+ * TSS_EINVAL (bad cfg, NULL buffer), TSS_ENOSPACE (buffer too small),
+ * TSS_EHIP.  Paper: Method / Domain-Aware Skip Controller (one loaded target
+ * serves every domain; all parameters stay loaded). */
 int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, size_t weights_bytes,
                void* dev_workspace, size_t workspace_bytes, tss_ctx** out);
 
@@ -139,25 +147,45 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
  *       w_down [d][ffn]
  *   1 + 9*n_layers: final_norm [d];   2 + 9*n_layers: lm_head [vocab][d]
  * Returns when the copies are complete. */
+/* Paper: Appendix / Models (LLaMA blocks: attention and SwiGLU MLP
+ * weights, RMSNorm gains, untied lm_head).  TSS_EINVAL for a range outside
+ * the list or a NULL tensor; TSS_EHIP poisons the context. */
 int tss_load_weights(tss_ctx* ctx, int32_t first, int32_t count, const void* const* host_tensors);
 
 /* Binds a KV pool of tss_kv_bytes(cfg, n_seqs, max_tokens_per_seq) bytes of
- * device memory and resets every sequence to length 0.  page_order, if not
- * NULL, lists a permutation of the pool's n_seqs * ceil(max_tokens/16) pages;
- * sequence s owns the s-th run of pages in that order (NULL = identity). */
+ * device memory and resets every sequence to length 0 (masks to dense).
+ * page_order, if not NULL, lists a permutation of the pool's
+ * n_seqs * ceil(max_tokens/16) pages; sequence s owns the s-th run of pages
+ * in that order (NULL = identity); TSS_EINVAL if it is not a permutation.
+ * Rebinding (the same or another pool) is allowed at any time: steps
+ * captured for the previous binding are discarded.  The caller owns the
+ * pool.  Paper: Problem Formulation (the drafts are verified against the
+ * committed prefix, whose keys and values the underlying method caches). */
 int tss_kv_alloc(tss_ctx* ctx, int32_t n_seqs, int32_t max_tokens_per_seq, void* dev_pool, size_t pool_bytes,
                  const int32_t* page_order);
 
 /* Sets the skip mask of a sequence (n_layers bytes of 0/1; NULL = dense).
- * The mask is the sequence's default for prefill and verify. */
+ * The mask is the sequence's default for prefill and verify.  TSS_EINVAL for
+ * an unknown sequence or a byte other than 0/1.  Paper: Method /
+ * Domain-Aware Skip Controller (the skip set of the request's domain, fixed
+ * for the whole request; the empty set for unsupported domains). */
 int tss_set_skip_mask(tss_ctx* ctx, int32_t seq, const uint8_t* mask);
 
 /* Appends n context tokens to sequence seq under its skip mask: their K/V are
  * computed and kept for every layer the mask runs.  The tokens go through the
- * decoder in chunks of min(64, rows of one step). */
+ * decoder in chunks of min(64, rows of one step).  TSS_ECAPACITY past the
+ * sequence's capacity, TSS_ESTATE if an active layer lacks K/V for the
+ * committed context.  Paper: Method / Domain-Aware Skip Controller (the same
+ * block rule in the target's forward for every token of the request). */
 int tss_prefill(tss_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n);
 
-/* One verification step.
+/* One verification step.  Paper: Method / Problem Formulation (the target
+ * verifies the drafted tokens in one parallel pass; T_S bypasses the blocks
+ * of S), Method / Domain-Aware Skip Controller (the per-block membership
+ * check: a skipped block passes its hidden state through, with no attention
+ * or feed-forward work), Experiments / Models and speculative decoding
+ * methods and Appendix / Evaluation Protocol (greedy acceptance, temperature
+ * 0, the underlying method's accept rule unchanged).
  *   draft_tokens[n_nodes]: node 0 is the root (the last committed token,
  *     whose K/V are not cached yet); nodes 1.. are drafted tokens.
  *   tree_parent[n_nodes]: parent[0] = -1 and 0 <= parent[i] < i; NULL = chain.
@@ -173,7 +201,9 @@ int tss_prefill(tss_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n);
 int tss_verify(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent, int32_t n_nodes,
                const uint8_t* skip_mask, uint32_t flags, int32_t* accept_len, int32_t* next_token);
 
-/* Verifies several sequences in one step (the same forward as tss_verify, on
+/* Paper: as tss_verify, for several requests, each with its own domain's
+ * skip set (Domain-Aware Skip Controller).
+ * Verifies several sequences in one step (the same forward as tss_verify, on
  * the rows of every sequence at once, so each active block's weights are read
  * once for the whole batch).
  *   seq_ids[n_seqs]: distinct sequences.
@@ -229,18 +259,31 @@ int tss_verify_sweep(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, con
                      int32_t n_nodes, int32_t n_masks, const uint8_t* skip_masks, int32_t* accept_len,
                      int32_t* next_token, int32_t* greedy, void* dev_prefix, size_t prefix_bytes);
 
-/* Bytes of the prefix buffer of tss_verify_sweep for trees of n_nodes nodes:
+/* Paper: Algorithm 1 (the evaluations of the search).
+ * Bytes of the prefix buffer of tss_verify_sweep for trees of n_nodes nodes:
  * n_layers * n_nodes * d_model fp32 values (0 when cfg or n_nodes is
  * invalid). */
 size_t tss_sweep_prefix_bytes(const tss_model_cfg* cfg, int32_t n_nodes);
 
 /* Copies the last verify's fp32 logits [n_nodes][vocab] / greedy tokens
- * [n_nodes] to host memory (rows in the step's node order).  n_nodes must not
- * exceed the last verify's node count (all sequences of a batch). */
+ * [n_nodes] to host memory (rows in the step's node order); returns when the
+ * copy is done.  n_nodes must not exceed the last verify's node count (all
+ * sequences of a batch; TSS_EINVAL otherwise).  Paper: Experiments / Models
+ * and speculative decoding methods (the greedy tokens the accept rule
+ * compares the drafts with). */
 int tss_get_logits(tss_ctx* ctx, float* host_dst, int32_t n_nodes);
 int tss_get_greedy(tss_ctx* ctx, int32_t* host_dst, int32_t n_nodes);
 
-/* Accepted path of result i of the last verify (i = the sequence's index in
+/* Enqueues on the context's stream a copy of the last verify's fp32 logits
+ * [n_nodes][vocab] into dev_dst, device memory of at least n_nodes * vocab
+ * floats owned by the caller, and returns without waiting (the copy is
+ * ordered before any later work on that stream).  TSS_EINVAL as for
+ * tss_get_logits.  Paper: as tss_get_logits. */
+int tss_get_logits_device(tss_ctx* ctx, float* dev_dst, int32_t n_nodes);
+
+/* Paper: Experiments / Models and speculative decoding methods (the accepted
+ * draft path that the underlying method commits).
+ * Accepted path of result i of the last verify (i = the sequence's index in
  * the batch, 0 for tss_verify; for tss_verify_sweep, the mask's index in the
  * last step): path_nodes[0 .. *path_len) = local node ids from the root to
  * the deepest accepted node, *path_len = accept_len + 1.  With TSS_COMMIT
@@ -248,18 +291,22 @@ int tss_get_greedy(tss_ctx* ctx, int32_t* host_dst, int32_t n_nodes);
  * path_nodes must hold max_nodes entries. */
 int tss_get_path(tss_ctx* ctx, int32_t index, int32_t* path_nodes, int32_t* path_len);
 
-/* Committed length of a sequence, and rewinding it (n_kv <= current length). */
+/* Committed length of a sequence, and rewinding it (n_kv <= current length;
+ * TSS_EINVAL otherwise).  Paper: Problem Formulation (the committed prefix). */
 int tss_seq_length(tss_ctx* ctx, int32_t seq, int32_t* n_kv);
 int tss_seq_truncate(tss_ctx* ctx, int32_t seq, int32_t n_kv);
 
-/* Pure host checks, the same code the calls above run. */
+/* Pure host checks, the same code the calls above run.  Paper: Problem
+ * Formulation (draft trees: each node's parent precedes it; the skip set is
+ * a subset of the blocks). */
 int tss_validate_tree(const int32_t* parent, int32_t n_nodes, int32_t max_nodes);
 int tss_validate_mask(const uint8_t* mask, int32_t n_layers);
 /* depth[i] and anc[i] (bit j set iff node j is i or an ancestor of i). */
 int tss_tree_meta(const int32_t* parent, int32_t n_nodes, int32_t* depth, uint64_t* anc);
 
 /* Selects the launch mode of tss_verify (enum tss_launch_mode).  At most 32
- * captured step shapes are kept per context (least recently used dropped). */
+ * captured step shapes are kept per context (least recently used dropped).
+ * Runtime plumbing; no passage of the paper. */
 int tss_set_launch_mode(tss_ctx* ctx, int32_t mode);
 
 /* Times one kernel launch per verify: the launch of kind `kernel` (enum
@@ -273,6 +320,25 @@ int tss_set_launch_mode(tss_ctx* ctx, int32_t mode);
  * (reset != 0 clears them). */
 int tss_profile_kernel(tss_ctx* ctx, int32_t kernel, int32_t layer);
 int tss_profile_read(tss_ctx* ctx, double* total_ms, int64_t* count, int32_t reset);
+
+/* How the last step (verify, sweep step or prefill chunk) divided the
+ * attention of its last launched block: *n_items attention items (runs of at
+ * most 64 consecutive rows of one KV sequence), and for item i the number of
+ * workgroups per head its context pages were split among (groups[i]; 1 = no
+ * cross-workgroup merge) and its rows (rows[i]).  groups and rows must hold
+ * 16 entries.  *n_items = 0 when the step launched no block.  Waits for the
+ * context's stream.  Inspection only (tests assert with it which attention
+ * path a launch took); no passage of the paper. */
+int tss_get_attn_split(tss_ctx* ctx, int32_t* n_items, int32_t* groups, int32_t* rows);
+
+/* Consistency check of the KV binding, a debugging aid (it waits for the
+ * context's stream and copies the page table back): the page table is a
+ * permutation of the pool's pages (every entry inside the pool, none owned
+ * twice), the device copy equals the host's, and every sequence's committed
+ * length and per-layer K/V lengths stay within its capacity.  TSS_OK,
+ * TSS_ESTATE naming the first inconsistency (tss_last_error), or TSS_EHIP.
+ * No passage of the paper. */
+int tss_check_kv(tss_ctx* ctx);
 
 /* Message of the context's last failure; with ctx = NULL, of the calling
  * thread's last failed tss_create. */

@@ -152,6 +152,11 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   // few enough that partial states (T tiles each) stay well below the pages
   const int cap = a.pages_per_wg > 0 ? min(a.groups, (n_pages + a.pages_per_wg - 1) / a.pages_per_wg) : a.groups;
   const int G = max(1, min(cap, min((n_pages + W - 1) / W, n_pages / (TSS_ATTN_PART_DIV * T))));
+  if (head == 0 && g == 0 && threadIdx.x == 0) {  // the split this launch took (inspection)
+    a.split_out[y] = G;
+    a.split_out[kAttnMaxItems + y] = Ms;
+    if (y == 0) a.split_out[2 * kAttnMaxItems] = (int)gridDim.y;
+  }
   if (g >= G) {                                      // uniform over the workgroup
     __builtin_amdgcn_s_waitcnt(0);                   // let the early page load land first
     return;

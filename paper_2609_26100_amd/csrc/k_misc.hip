@@ -21,6 +21,8 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     const uint32_t* src = (const uint32_t*)&a.sp;
     uint32_t* dst = (uint32_t*)a.sp_dev;
     for (int i = threadIdx.x; i < (int)(sizeof(StepParams) / 4); i += 256) dst[i] = src[i];
+    // a step whose blocks are all skipped reports no attention items
+    if (threadIdx.x == 0) a.attn_split[2 * kAttnMaxItems] = 0;
   }
   const float* gain = a.gain[a.sp.row_seq[m]];
   // Each thread takes whole 16-column parts (up to two; d <= 8192): the

@@ -43,8 +43,8 @@ struct WeightLayout {
 };
 
 struct WsLayout {
-  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, counters, kpart, kcount, logits, am_val,
-      am_idx, greedy, total;
+  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, counters, attn_split, kpart, kcount, logits,
+      am_val, am_idx, greedy, total;
 };
 
 // weight element bytes; the KV cache uses the same width (fp16 in the bf16
@@ -138,6 +138,7 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   w.part_o = take(slots * kAttnMaxTiles * 16 * c->head_dim * 4);
   w.part_ml = take(slots * kAttnMaxTiles * 16 * 2 * 4);
   w.counters = take((size_t)c->n_heads * kAttnMaxItems * 4);
+  w.attn_split = take((2 * kAttnMaxItems + 1) * 4);
   w.kpart = take((size_t)kMaxKSplit * d * Mp * 4);  // K-split partial products of the residual projections
   w.kcount = take((d / 16) * 4);
   w.logits = take(Mp * v * 4);
@@ -239,6 +240,21 @@ std::string& create_error() {
 int fail(tss_ctx* c, int code, const std::string& msg) {
   if (c) c->err = msg;
   return code;
+}
+
+// Destroys every captured verify step.  A captured step holds the addresses
+// the KV binding gave it (pool pages, page table, per-sequence page-table
+// offsets, the first page ids, the rotary table), so a rebind must drop them
+// all; the next verify of each shape captures it again.
+hipError_t drop_graphs(tss_ctx* c) {
+  hipError_t first = hipSuccess;
+  for (auto& g : c->graphs) {
+    const hipError_t a = g.exec ? hipGraphExecDestroy(g.exec) : hipSuccess;
+    const hipError_t b = g.graph ? hipGraphDestroy(g.graph) : hipSuccess;
+    if (first == hipSuccess) first = a != hipSuccess ? a : b;
+  }
+  c->graphs.clear();
+  return first;
 }
 
 int hip_fail(tss_ctx* c, hipError_t e, const char* where) {
@@ -419,10 +435,7 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
 
 void tss_destroy(tss_ctx* c) {
   if (!c) return;
-  for (auto& g : c->graphs) {
-    if (g.exec) (void)hipGraphExecDestroy(g.exec);
-    if (g.graph) (void)hipGraphDestroy(g.graph);
-  }
+  (void)drop_graphs(c);
   if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
   for (int i = 0; i < 2; ++i) {
     if (c->stage_ev[i]) {
@@ -569,6 +582,7 @@ int tss_kv_alloc(tss_ctx* c, int32_t n_seqs, int32_t max_tokens_per_seq, void* d
     for (int i = 0; i < k.n_pages; ++i) pt[i] = i;
   }
   HIPCHK(hipStreamSynchronize(c->stream), "sync before KV bind");
+  HIPCHK(drop_graphs(c), "dropping the steps captured for the previous KV binding");
   c->kv = (uint8_t*)dev_pool;
   c->kvl = k;
   c->n_seqs = n_seqs;
@@ -819,6 +833,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
       a.part_o = (float*)(ws + c->wsl.part_o);
       a.part_ml = (float*)(ws + c->wsl.part_ml);
       a.counters = (int*)(ws + c->wsl.counters);
+      a.split_out = (int32_t*)(ws + c->wsl.attn_split);
       if (!one_seq && n_act > 1) {
         a.groups = attn_batch_groups(H, n_act, pps);
         a.pages_per_wg = kAttnPagesPerWG;
@@ -991,6 +1006,7 @@ EmbedArgs embed_args(tss_ctx* c, int start_layer, const float* src_h) {
   a.ss_stride = cf.d_model / 16;
   a.d = cf.d_model;
   a.M = sp.M;
+  a.attn_split = (int32_t*)(c->ws + c->wsl.attn_split);
   return a;
 }
 
@@ -1398,6 +1414,59 @@ int tss_get_path(tss_ctx* c, int32_t index, int32_t* path_nodes, int32_t* path_l
   const Result& r = c->res_host[index];
   *path_len = r.path_len;
   for (int i = 0; i < r.path_len; ++i) path_nodes[i] = r.path[i];
+  return TSS_OK;
+}
+
+int tss_get_logits_device(tss_ctx* c, float* dev_dst, int32_t n_nodes) {
+  if (!c || !dev_dst) return TSS_EINVAL;
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  if (n_nodes < 1 || n_nodes > c->last_M) return fail(c, TSS_EINVAL, "n_nodes exceeds the last verify's nodes");
+  HIPCHK(hipMemcpyAsync(dev_dst, c->ws + c->wsl.logits, (size_t)n_nodes * c->cfg.vocab * 4, hipMemcpyDeviceToDevice,
+                        c->stream),
+         "logits copy");
+  return TSS_OK;
+}
+
+int tss_get_attn_split(tss_ctx* c, int32_t* n_items, int32_t* groups, int32_t* rows) {
+  if (!c || !n_items || !groups || !rows) return TSS_EINVAL;
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  int32_t rep[2 * kAttnMaxItems + 1];
+  HIPCHK(hipStreamSynchronize(c->stream), "sync");
+  HIPCHK(hipMemcpy(rep, c->ws + c->wsl.attn_split, sizeof(rep), hipMemcpyDeviceToHost), "split copy");
+  const int n = std::max(0, std::min(rep[2 * kAttnMaxItems], kAttnMaxItems));
+  *n_items = n;
+  for (int i = 0; i < n; ++i) {
+    groups[i] = rep[i];
+    rows[i] = rep[kAttnMaxItems + i];
+  }
+  return TSS_OK;
+}
+
+int tss_check_kv(tss_ctx* c) {
+  if (!c) return TSS_EINVAL;
+  if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
+  if (!c->kv) return fail(c, TSS_ESTATE, "no KV pool bound (tss_kv_alloc)");
+  const int np = c->kvl.n_pages;
+  if ((int)c->pt_host.size() != np) return fail(c, TSS_ESTATE, "host page table has the wrong length");
+  std::vector<uint8_t> seen(np, 0);
+  for (int i = 0; i < np; ++i) {
+    const int p = c->pt_host[i];
+    if (p < 0 || p >= np) return fail(c, TSS_ESTATE, "page table entry " + std::to_string(i) + " outside the pool");
+    if (seen[p]++) return fail(c, TSS_ESTATE, "page " + std::to_string(p) + " owned twice");
+  }
+  std::vector<int32_t> dev(np);
+  HIPCHK(hipStreamSynchronize(c->stream), "sync");
+  HIPCHK(hipMemcpy(dev.data(), c->kv + c->kvl.page_table, (size_t)np * 4, hipMemcpyDeviceToHost), "page table copy");
+  for (int i = 0; i < np; ++i)
+    if (dev[i] != c->pt_host[i])
+      return fail(c, TSS_ESTATE, "device page table differs from the host copy at entry " + std::to_string(i));
+  for (int s = 0; s < c->n_seqs; ++s) {
+    if (c->n_kv[s] < 0 || c->n_kv[s] > c->max_tokens)
+      return fail(c, TSS_ESTATE, "sequence " + std::to_string(s) + " length outside its capacity");
+    for (int l = 0; l < c->cfg.n_layers; ++l)
+      if (c->kv_len[s][l] < 0 || c->kv_len[s][l] > c->n_kv[s])
+        return fail(c, TSS_ESTATE, "sequence " + std::to_string(s) + " holds K/V past its length");
+  }
   return TSS_OK;
 }
 

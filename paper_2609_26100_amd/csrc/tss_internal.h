@@ -223,6 +223,9 @@ struct AttnArgs {
   float* part_o;           // [slots][kAttnMaxTiles][16][hd] unnormalised partial outputs
   float* part_ml;          // [slots][kAttnMaxTiles][16][2] (max in log2 units, sum)
   int* counters;           // [H * kAttnMaxItems] arrivals, zero between launches
+  // report of the launch's split: per item the workgroups G its pages were
+  // divided among and its rows, then the item count ([2 * kAttnMaxItems + 1])
+  int32_t* split_out;
   int groups;              // most workgroups per (head, item)
   int pages_per_wg;        // > 0: an item takes ceil(pages / pages_per_wg) workgroups (at most groups)
   int layer, n_pages_pool, n_heads, d;
@@ -252,6 +255,7 @@ struct EmbedArgs {
   float* ss_out;           // [M][ss_stride]: sums of h^2 over 16-column parts
   int ss_stride;
   int d, M;
+  int32_t* attn_split;     // the attention split report (AttnArgs::split_out): its item count is cleared
 };
 
 struct AcceptArgs {

@@ -28,7 +28,7 @@ EXPORTS = (
     "tss_load_weights", "tss_kv_alloc", "tss_set_skip_mask", "tss_prefill", "tss_verify", "tss_get_logits",
     "tss_verify_batch", "tss_verify_sweep", "tss_sweep_prefix_bytes", "tss_get_greedy", "tss_get_path", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
     "tss_tree_meta", "tss_set_launch_mode", "tss_profile_kernel", "tss_profile_read", "tss_last_error", "tss_status_string",
-    "tss_destroy",
+    "tss_destroy", "tss_get_logits_device", "tss_get_attn_split", "tss_check_kv",
 )
 
 
@@ -75,6 +75,9 @@ def lib():
             "tss_sweep_prefix_bytes": (SZ, [CFG, I32]),
             "tss_get_logits": (ctypes.c_int, [P, P, I32]),
             "tss_get_greedy": (ctypes.c_int, [P, P, I32]),
+            "tss_get_logits_device": (ctypes.c_int, [P, P, I32]),
+            "tss_get_attn_split": (ctypes.c_int, [P, ctypes.POINTER(I32), P, P]),
+            "tss_check_kv": (ctypes.c_int, [P]),
             "tss_get_path": (ctypes.c_int, [P, I32, P, ctypes.POINTER(I32)]),
             "tss_seq_length": (ctypes.c_int, [P, I32, ctypes.POINTER(I32)]),
             "tss_seq_truncate": (ctypes.c_int, [P, I32, I32]),
@@ -221,6 +224,24 @@ def tss_get_logits(ctx, n_nodes, vocab):
     out = np.empty((n_nodes, vocab), dtype=np.float32)
     _check(lib().tss_get_logits(ctx, _ptr(out), n_nodes), ctx, "tss_get_logits")
     return out
+
+
+def tss_get_logits_device(ctx, dev_dst, n_nodes):
+    """Enqueues a copy of the last verify's logits into device memory at dev_dst (an address)."""
+    _check(lib().tss_get_logits_device(ctx, dev_dst, n_nodes), ctx, "tss_get_logits_device")
+
+
+def tss_get_attn_split(ctx):
+    """[(groups, rows)] per attention item of the last step's last attention launch."""
+    n = ctypes.c_int32()
+    groups = np.zeros(16, dtype=np.int32)
+    rows = np.zeros(16, dtype=np.int32)
+    _check(lib().tss_get_attn_split(ctx, ctypes.byref(n), _ptr(groups), _ptr(rows)), ctx, "tss_get_attn_split")
+    return [(int(groups[i]), int(rows[i])) for i in range(n.value)]
+
+
+def tss_check_kv(ctx):
+    _check(lib().tss_check_kv(ctx), ctx, "tss_check_kv")
 
 
 def tss_get_greedy(ctx, n_nodes):

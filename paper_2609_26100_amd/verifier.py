@@ -36,6 +36,18 @@ class Verifier:
         self._mask = {i: np.zeros(shape.n_layers, np.uint8) for i in range(n_seqs)}
         self.prefix = None  # device buffer of the mask sweep's shared prefix
 
+    def bind_kv(self, n_seqs, max_tokens, page_order=None):
+        """Binds a new KV pool (a new device buffer) and resets every sequence to length 0 with a dense
+        mask.  Returns the previous pool's tensor: the library no longer touches it."""
+        kb = abi.tss_kv_bytes(self.cfg, n_seqs, max_tokens)
+        old = self.kv_pool
+        self.kv_pool = self.torch.zeros(kb, dtype=self.torch.uint8, device=self.device)
+        self.torch.cuda.synchronize(self.device)
+        abi.tss_kv_alloc(self.ctx, n_seqs, max_tokens, self.kv_pool.data_ptr(), kb, page_order)
+        self.n_seqs, self.max_tokens = n_seqs, max_tokens
+        self._mask = {i: np.zeros(self.shape.n_layers, np.uint8) for i in range(n_seqs)}
+        return old
+
     def load(self, get_tensor):
         """Streams every tensor, in the ABI's tensor order, from get_tensor(index) -> host array in the
         shape's dtype (fp32, or bf16 bit patterns as uint16)."""
@@ -92,6 +104,20 @@ class Verifier:
 
     def logits(self, n_nodes):
         return abi.tss_get_logits(self.ctx, n_nodes, self.shape.vocab)
+
+    def logits_device(self, n_nodes):
+        """The last verify's logits copied into a new torch device tensor [n_nodes][vocab] on the verifier's stream."""
+        out = self.torch.empty((n_nodes, self.shape.vocab), dtype=self.torch.float32, device=self.device)
+        abi.tss_get_logits_device(self.ctx, out.data_ptr(), n_nodes)
+        return out
+
+    def check_kv(self):
+        """Raises if the KV binding is inconsistent (page table, lengths)."""
+        abi.tss_check_kv(self.ctx)
+
+    def attn_split(self):
+        """[(workgroups per head, rows)] per attention item of the last step's last attention launch."""
+        return abi.tss_get_attn_split(self.ctx)
 
     def greedy(self, n_nodes):
         return abi.tss_get_greedy(self.ctx, n_nodes)
