@@ -63,3 +63,33 @@ def compare_step(shape, v, seq, m, oseq, tokens, parent=None, mask=None, commit=
     np.testing.assert_array_equal(g[sure], res.greedy[sure])
     compared = check_decision(res, al, nt, gate)
     return res, (al, nt), err, compared
+
+
+def prefill_chunked(m, oseq, tokens, chunk=512):
+    """The oracle's prefill in pieces of `chunk` tokens (the same chain, bounded score arrays)."""
+    tokens = np.asarray(tokens)
+    for i in range(0, len(tokens), chunk):
+        prefill(m, oseq, tokens[i:i + chunk])
+
+
+def oracle_tree_tokens(m, oseq, parent, root, vocab, p_accept, stream, mask=None):
+    """Draft-tree tokens whose accepted branches follow the oracle's greedy tokens (synth.tree_draft_tokens
+    with the oracle as the target)."""
+    parent = np.asarray(parent)
+
+    def greedy_of(tok, node):
+        path = [node]
+        while parent[path[-1]] >= 0:
+            path.append(int(parent[path[-1]]))
+        return int(verify(m, oseq, tok[path[::-1]], None, mask).greedy[-1])
+    return synth.tree_draft_tokens(parent, root, greedy_of, vocab, p_accept, stream=stream)
+
+
+def assert_merged_split(v, rows, min_groups=2):
+    """The last step's last attention launch divided every listed item's context pages among at least
+    min_groups workgroups per head (the cross-workgroup merge path); rows = expected rows per item."""
+    split = v.attn_split()
+    log(f"attention split (workgroups per head, rows) per item: {split}")
+    assert [r for _, r in split] == list(rows), split
+    assert all(g >= min_groups for g, _ in split), split
+    return split

@@ -3,9 +3,12 @@ configuration the benchmark times (k=5 chains, 1024-token paged context).
 
 * Full depth against the oracle: all 32 layers (dense and the 8-layer skip
   mask), element-wise logits and the accept decision, at a 64-token context
-  (the oracle's fp32 prefill of 1024 tokens through 32 layers is too slow for a
+  (one attention workgroup per head) and, dense, at a 512-token context,
+  where each head's pages are split among five workgroups whose partial
+  states are merged across workgroups as at the benchmark's 1024 tokens (the
+  oracle's fp32 prefill of 1024 tokens through 32 layers is too slow for a
   test; every kernel's launch shape except the attention split count is the
-  same at 64 and 1024 tokens).
+  same at 512 and 1024 tokens).
 * At the benchmark's 1024-token context, properties that hold at any size:
   the target's own greedy drafts are fully accepted, steps are bit-exact run
   to run, a chain passed as an explicit parent array is bit-exact with the
@@ -17,7 +20,7 @@ import pytest
 
 import synth
 from oracle import OracleSequence, prefill, verify
-from tests.gpu_common import compare_step, gpu_verifier, log, oracle_model
+from tests.gpu_common import assert_merged_split, compare_step, gpu_verifier, log, oracle_model, prefill_chunked
 
 pytestmark = pytest.mark.gpu
 
@@ -64,6 +67,34 @@ def test_full_depth_vs_oracle(gpu, oracle7b, skips):
         worst = max(worst, err)
         log(f"32 layers skip {skips} root {r}: accept {al}/{res.accept_len} next {nt}/{res.next_token} err {err:.3e}")
     log(f"32 layers skip {skips}: worst logits max-abs {worst:.3e}, {compared}/3 decisions compared")
+    assert compared >= 1
+
+
+def test_full_depth_vs_oracle_ctx512(gpu, oracle7b):
+    v, m = gpu, oracle7b
+    mask = MASKS[0]
+    n = 512
+    toks = synth.context_tokens(SHAPE.vocab, n + 4, stream=36)
+    v.truncate(1, 0)
+    v.set_mask(1, mask)
+    v.prefill(1, toks[:n])
+    o = OracleSequence(m, mask)
+    prefill_chunked(m, o, toks[:n], chunk=256)
+    compared, worst = 0, 0.0
+    for r in range(2):
+        root = int(toks[n + r])
+        g, cur = [], [root]
+        for _ in range(5):
+            g.append(int(verify(m, o, np.asarray(cur)).greedy[-1]))
+            cur.append(g[-1])
+        drafts = synth.chain_draft(np.asarray(g), SHAPE.vocab, p_accept=0.6, stream=40 + r)
+        res, (al, nt), err, c = compare_step(SHAPE, v, 1, m, o, np.concatenate([[root], drafts]))
+        assert_merged_split(v, [6])
+        compared += c
+        worst = max(worst, err)
+        log(f"32 layers at 512 tokens root {r}: accept {al}/{res.accept_len} next {nt}/{res.next_token} "
+            f"err {err:.3e}")
+    log(f"32 layers at 512 tokens: worst logits max-abs {worst:.3e}, {compared}/2 decisions compared")
     assert compared >= 1
 
 

@@ -16,7 +16,7 @@ import pytest
 
 import synth
 from oracle import OracleSequence, prefill, verify
-from tests.gpu_common import TOL, check_decision, gpu_verifier, log, oracle_model
+from tests.gpu_common import TOL, check_decision, gpu_verifier, log, oracle_model, prefill_chunked
 
 pytestmark = pytest.mark.gpu
 
@@ -32,7 +32,7 @@ def _setup(v, m, shape, seqs, masks, ctx_lens, stream0):
         v.set_mask(sq, mask)
         v.prefill(sq, ctx)
         o = OracleSequence(m, mask)
-        prefill(m, o, ctx)
+        prefill_chunked(m, o, ctx)
         oseqs.append(o)
     return oseqs
 
@@ -223,3 +223,44 @@ def test_13b_dims_batch_of_8_vs_oracle():
         log(f"13B dims batch rep {rep}: accept {list(al)}, logits err {err:.3e}, compared {c}/8")
     v.close()
     assert comp >= 8
+
+
+# 2 blocks with 13B dimensions and room for 4160 tokens per sequence: a batch
+# whose contexts exceed 1024 tokens takes one attention workgroup per 64 pages
+# of each sequence, merged across workgroups (the path of the 13B batch
+# workload, contexts 512-4096)
+SHAPE13_2 = dataclasses.replace(synth.LLAMA_13B, n_layers=2, name="llama13b-2l")
+
+
+def test_13b_dims_batch_long_contexts_vs_oracle():
+    log("building the 2-layer 13B-dimension bf16 model (batch of 8 x 9 nodes, 4160 tokens per sequence)")
+    v = gpu_verifier(SHAPE13_2, n_seqs=8, max_tokens=4160, max_nodes=9, max_batch=8)
+    m = oracle_model(SHAPE13_2)
+    seqs = list(range(8))
+    ctx_lens = [1100, 2100, 64, 300, 1300, 40, 200, 520]
+    # the long contexts run both blocks; the others skip one block or none
+    skips = [[], [], [0], [1], [], [1], [0], []]
+    masks = [synth.mask_from_layers(2, sk) for sk in skips]
+    log(f"contexts {ctx_lens}, skipped blocks {skips}")
+    oseqs = _setup(v, m, SHAPE13_2, seqs, masks, ctx_lens, 1700)
+    drafts = []
+    for i, o in enumerate(oseqs):
+        root = int(synth.context_tokens(SHAPE13_2.vocab, 1, stream=1800 + i)[0])
+        g, cur = [], [root]
+        for _ in range(8):
+            g.append(int(verify(m, o, np.asarray(cur)).greedy[-1]))
+            cur.append(g[-1])
+        drafts.append(np.concatenate([[root], synth.chain_draft(np.asarray(g), SHAPE13_2.vocab, p_accept=0.6,
+                                                                stream=1900 + i)]))
+    err, comp, (al, nt) = _compare_batch(SHAPE13_2, v, m, seqs, oseqs, drafts, None)
+    # the last launched block (1) serves the sequences that run it, one item each
+    split = v.attn_split()
+    log(f"13B dims long batch: accept {list(al)}, logits err {err:.3e}, compared {comp}/8; split {split}")
+    runs1 = [i for i in seqs if 1 not in skips[i]]
+    assert [r for _, r in split] == [9] * len(runs1)
+    groups = dict(zip(runs1, [gr for gr, _ in split]))
+    assert all(groups[i] >= 2 for i in (0, 1, 4)), groups
+    assert groups[1] > groups[0], groups
+    v.check_kv()
+    v.close()
+    assert comp >= 4

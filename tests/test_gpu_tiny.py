@@ -343,3 +343,67 @@ def test_nan_logits_pick_the_first_nan():
         assert float(np.max(np.abs(lg[finite] - res.logits[finite]))) <= 1e-4
     finally:
         v.close()
+
+
+def test_kv_rebind_drops_captured_steps():
+    """Steps captured for one KV binding must not survive a rebind: after
+    verifies have been captured and replayed, the context is rebound to a new
+    pool (another size, permuted pages) and the old pool is filled with a
+    sentinel.  Prefill and verify (chain and tree) on the new pool must equal
+    a fresh context bit for bit, and the old pool must stay untouched."""
+    import torch
+    v = gpu_verifier(SHAPE, random_gains=True, n_seqs=2, max_tokens=200, max_nodes=16)
+    w = gpu_verifier(SHAPE, random_gains=True, n_seqs=3, max_tokens=300, max_nodes=16)
+    ctx = synth.context_tokens(SHAPE.vocab, 90, stream=61)
+    chain = synth.context_tokens(SHAPE.vocab, 6, stream=62)
+    tree = synth.random_tree(9, stream=63, max_children=3)
+    tree_tok = synth.context_tokens(SHAPE.vocab, 9, stream=64)
+    for sq in (0, 1):
+        v.prefill(sq, ctx[: 40 + 20 * sq])
+    for _ in range(3):  # capture, then replay, both step shapes on both sequences
+        for sq in (0, 1):
+            v.verify(sq, chain)
+            v.verify(sq, tree_tok, tree)
+    n_pages = 3 * ((300 + 15) // 16)
+    perm = np.random.default_rng(65).permutation(n_pages).astype(np.int32)
+    old = v.bind_kv(3, 300, perm)
+    old.fill_(0x7F)
+    torch.cuda.synchronize()
+    results = {}
+    for name, x in (("rebound", v), ("fresh", w)):
+        out = []
+        for sq in (2, 1):
+            x.prefill(sq, ctx[: 50 + 20 * sq])
+            out.append((x.verify(sq, chain), x.logits(6)))
+            out.append((x.verify(sq, tree_tok, tree, commit=True), x.logits(9)))
+            out.append((x.verify(sq, chain), x.logits(6)))
+        results[name] = out
+    for (da, la), (db, lb) in zip(results["rebound"], results["fresh"]):
+        assert da == db
+        np.testing.assert_array_equal(la, lb)
+    assert v.length(1) == w.length(1) and v.length(2) == w.length(2)
+    assert bool((old == 0x7F).all()), "a step wrote into the KV pool of the previous binding"
+    v.check_kv()
+    w.check_kv()
+    v.close()
+    w.close()
+
+
+def test_logits_device_copy_and_split_report(pair):
+    """tss_get_logits_device gives the host copy's values; the attention split
+    report names one workgroup per head at a short context and no item when
+    every block is skipped."""
+    v, m = pair
+    mask = synth.mask_from_layers(L, [2])
+    ctx = synth.context_tokens(SHAPE.vocab, 30, stream=66)
+    o = _fresh(v, m, 2, mask, ctx)
+    tok = synth.context_tokens(SHAPE.vocab, 6, stream=67)
+    v.verify(2, tok)
+    host = v.logits(6)
+    dev = v.logits_device(6)
+    np.testing.assert_array_equal(dev.cpu().numpy(), host)
+    assert v.attn_split() == [(1, 6)]
+    v.verify(2, tok, mask=np.ones(L, np.uint8))
+    assert v.attn_split() == []
+    res = verify(m, o, tok, mask=np.ones(L, np.uint8))
+    assert float(np.max(np.abs(v.logits(6) - res.logits))) <= 1e-4
