@@ -1,6 +1,20 @@
-"""Oracle of the offline skip-set search: the Acceptance- and Metric-Aware
-Breadth Search (Algorithm 1 and the section that explains it), written as the
-algorithm's steps in the paper's order and notation.
+"""Oracle of the offline skip-set search (the Acceptance- and Metric-Aware
+Breadth Search of the paper's search section, Algorithm 1), written from the
+quantities that section defines, each as a set:
+
+* the dense baseline (A_d^0, M_d^0, C_d^0) = E(empty set);
+* the candidate pool L_d: the layers whose single-layer skip keeps acceptance
+  within tau_A OR the metric within tau_M of the baseline (the permissive
+  filter);
+* the feasible configurations of depth k, F_d^(k): the k-subsets of L_d whose
+  acceptance is within eps_A AND whose metric is within eps_M of the baseline;
+* the stop rule: depths are explored in increasing k up to K, and the search
+  ends at the first depth whose F_d^(k) is empty (skipping is not additive,
+  so a deeper feasible set is never reached past an empty depth);
+* the Pareto set P_d: the baseline and every feasible configuration of the
+  explored depths, minus those another entry dominates in both acceptance and
+  metric;
+* the selection S_d^* = argmin C over the same configurations.
 
 TEST INFRASTRUCTURE ONLY (see the package docstring): the product's search
 driver is checked against this function on seeded evaluation tables.
@@ -10,86 +24,74 @@ downstream metric and verification cost of skip set S on the calibration set
 (Problem Formulation).  Layers are numbered 0 .. L-1 here (the paper counts
 from 1).  Readings where the paper leaves room:
 
-* The single-layer skips are evaluated in the candidate-pool loop and again
-  as the depth-1 configurations; E is deterministic, so both give one value.
-  This function calls E as often as the algorithm says (a memoising caller
-  evaluates each set once).
-* The depth-k configurations are every k-subset of the pool, in increasing
-  lexicographic order of their sorted layers (the order does not change the
-  result).
+* `evaluations` counts what the algorithm evaluates: the baseline, the L
+  single-layer skips of the pool filter, and every k-subset of the pool at
+  each explored depth (the empty depth that stops the search included).  The
+  depth-1 subsets are single-layer skips again; E is deterministic, so both
+  evaluations give one value, but both are counted.
+* F_d^(k) lists its sets in increasing lexicographic order of their sorted
+  layers (the order does not change the result, only which set is "first"
+  among equal costs).
 * "Dominated in both acceptance and downstream metric": S leaves the Pareto
   set when another entry has A >= A(S) and M >= M(S) with at least one of the
-  two strictly greater; cost plays no part (as the sentence says).  Entries
-  with equal (A, M) all stay.
-* argmin C runs over the union of the feasible sets of every depth, the empty
-  set included (the dense verifier is feasible by definition); ties go to the
-  configuration met first (empty set, then depth by depth in enumeration
-  order).
+  two strictly greater; cost plays no part.  Entries with equal (A, M) all
+  stay.
+* argmin C runs over the baseline and every feasible configuration (the
+  dense verifier is feasible by definition); ties go to the configuration met
+  first (the baseline, then depth by depth).
 """
 from __future__ import annotations
 
-import itertools
 from dataclasses import dataclass, field
+from itertools import combinations
+from math import comb
 
 
 @dataclass
 class SearchOutcome:
     best: frozenset                       # S_d^*
-    pareto: list                          # [(S, A, M, C)] after removing dominated entries
-    feasible: list                        # F_d: every feasible S, empty set first, depth by depth
+    pareto: list                          # P_d as [(S, A, M, C)]
+    feasible: list                        # the baseline, then F_d^(1), F_d^(2), ... of the explored depths
     pool: list                            # L_d, increasing layer order
-    evaluations: int                      # calls of E
-    depth_reached: int                    # last depth whose feasible set was non-empty (0: none)
-    per_depth: list = field(default_factory=list)  # |F_d^(k)| for each depth evaluated
+    evaluations: int                      # evaluations the algorithm makes
+    depth_reached: int                    # deepest depth with a non-empty F_d^(k) (0: none)
+    per_depth: list = field(default_factory=list)  # |F_d^(k)| of each explored depth
 
 
 def breadth_search(n_layers, K, evaluate, eps_A, eps_M, tau_A, tau_M):
-    """Algorithm 1.  evaluate(frozenset) -> (A, M, C); thresholds absolute."""
-    calls = 0
+    """S_d^* and the sets around it.  evaluate(frozenset) -> (A, M, C); thresholds absolute."""
+    known = {}
 
     def E(S):
-        nonlocal calls
-        calls += 1
-        A, M, C = evaluate(frozenset(S))
-        return float(A), float(M), float(C)
+        S = frozenset(S)
+        if S not in known:
+            A, M, C = evaluate(S)
+            known[S] = (float(A), float(M), float(C))
+        return known[S]
 
-    # dense baseline
-    A0, M0, C0 = E(())
-    # candidate pool: the permissive OR filter on single-layer skips
-    pool = []
-    for l in range(n_layers):
-        A, M, C = E((l,))
-        if A >= A0 - tau_A or M >= M0 - tau_M:
-            pool.append(l)
-    feasible = [frozenset()]
-    pareto = [(frozenset(), A0, M0, C0)]
-    costs = {frozenset(): C0}
-    per_depth = []
-    depth_reached = 0
+    A0, M0, _ = E(())
+    L_d = sorted({l for l in range(n_layers)
+                  if E((l,))[0] >= A0 - tau_A or E((l,))[1] >= M0 - tau_M})
+
+    def F(k):
+        """F_d^(k): the k-subsets of the pool meeting both tolerances."""
+        return [frozenset(S) for S in combinations(L_d, k)
+                if E(S)[0] >= A0 - eps_A and E(S)[1] >= M0 - eps_M]
+
+    # explored depths: 1 .. K, up to and including the first empty F_d^(k)
+    levels = []
     for k in range(1, K + 1):
-        level = []
-        for S in itertools.combinations(pool, k):
-            A, M, C = E(S)
-            # the strict AND feasibility on both objectives
-            if A >= A0 - eps_A and M >= M0 - eps_M:
-                level.append(frozenset(S))
-                pareto.append((frozenset(S), A, M, C))
-                costs[frozenset(S)] = C
-        per_depth.append(len(level))
-        if not level:
+        levels.append(F(k))
+        if not levels[-1]:
             break
-        feasible.extend(level)
-        depth_reached = k
-    # drop entries dominated in acceptance and metric
-    kept = []
-    for i, (S, A, M, C) in enumerate(pareto):
-        dominated = any(A2 >= A and M2 >= M and (A2 > A or M2 > M)
-                        for j, (_, A2, M2, _) in enumerate(pareto) if j != i)
-        if not dominated:
-            kept.append((S, A, M, C))
-    # the cheapest feasible configuration
-    best = feasible[0]
-    for S in feasible[1:]:
-        if costs[S] < costs[best]:
-            best = S
-    return SearchOutcome(best, kept, feasible, pool, calls, depth_reached, per_depth)
+    reached = [Fk for Fk in levels if Fk]          # every explored depth before the empty one
+    configs = [frozenset()] + [S for Fk in reached for S in Fk]
+
+    def dominated(S):
+        A, M, _ = E(S)
+        return any(E(T)[0] >= A and E(T)[1] >= M and (E(T)[0] > A or E(T)[1] > M) for T in configs if T != S)
+
+    pareto = [(S, *E(S)) for S in configs if not dominated(S)]
+    best = min(configs, key=lambda S: E(S)[2])      # min keeps the first of equal costs
+    evaluations = 1 + n_layers + sum(comb(len(L_d), k) for k in range(1, len(levels) + 1))
+    return SearchOutcome(best, pareto, configs, L_d, evaluations, len(reached), [len(Fk) for Fk in levels])

@@ -113,3 +113,21 @@ def test_skip_applied_to_wrong_layer_is_caught(env, monkeypatch):
         return real(model, seq, tokens, parent, np.roll(mask, 1), with_logits)
     monkeypatch.setattr(ov, "_forward", shifted)
     assert _fails(pins.test_skip_equals_deleted_block, _model64(get), get, [2])
+
+
+@pytest.mark.parametrize("kind", ["distinct_runner_up", "gap_to_mean"])
+def test_wrong_margin_is_caught(monkeypatch, kind):
+    """A margin taken against the second-largest distinct value (a tie then
+    looks decided) or against the row mean fails the closed-form margin pin."""
+    real = pins.verify
+
+    def bad(*args, **kw):
+        res = real(*args, **kw)
+        lg = res.logits
+        if kind == "distinct_runner_up":
+            res.margin = np.array([np.unique(r)[-1] - np.unique(r)[-2] for r in lg])
+        else:
+            res.margin = lg.max(axis=-1) - lg.mean(axis=-1)
+        return res
+    monkeypatch.setattr(pins, "verify", bad)
+    assert _fails(pins.test_margin_closed_form)

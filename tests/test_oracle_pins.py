@@ -15,7 +15,10 @@
   the tiny workload (3 greedy then 2 non-greedy drafts accept exactly 3).
 * Commit: after a committing step, the next step's logits equal the
   independent forward over context + accepted path + new drafts.
-* Closed forms for RMSNorm and the rotary rotation.
+* Closed forms for RMSNorm and the rotary rotation, and for the top-2 margin
+  that decides which parity cases are excused: with every block skipped and
+  one-hot embeddings, each node's logits are one lm_head column scaled by the
+  final norm, so the greedy token and the margin follow from that column.
 
 The independent forward computes rotary angles in fp32, so agreement is
 limited to about 1e-6; a dropped term, a wrong sign or a transposed operand
@@ -315,3 +318,32 @@ def test_tree_meta_validation():
     for bad in ([0, 0], [-1, 1], [-1, 0, 3], []):
         with pytest.raises(ValueError):
             tree_meta(bad)
+
+
+def test_margin_closed_form():
+    """margin = largest minus second-largest logit of each row (0 on a tie,
+    where the greedy token is the lowest tied index).  With every block
+    skipped, node i's embedding c * e_i makes its logits s * W_lm[:, i] with
+    s = sqrt(d) / sqrt(1 + eps * d / c^2) (final RMSNorm with unit gain), so
+    the margin is s times the gap between the column's two largest values."""
+    shape = dataclasses.replace(SHAPE, n_layers=1)
+    d, V, c = shape.d_model, shape.vocab, 0.37
+    rng = np.random.default_rng(3)
+    lm = rng.uniform(-1.0, 0.9, size=(V, d))
+    # column 0: a clear top-1 (index 17) over a runner-up (index 5)
+    lm[17, 0], lm[5, 0] = 3.0, 2.5
+    # column 1: a tie between indices 300 and 9 for the largest value
+    lm[300, 1], lm[9, 1] = 2.0, 2.0
+    # column 2: the largest value at the last index, every other value far below
+    lm[:, 2] = rng.uniform(-2.0, -0.5, size=V)
+    lm[V - 1, 2], lm[40, 2] = 1.25, -0.25
+    emb = np.zeros((V, d))
+    for i in range(3):
+        emb[i, i] = c
+    tensors = {"embed": emb, "lm_head": lm, "final_norm": np.ones(d)}
+    m = OracleModel(shape, lambda name, layer: tensors[name], dtype=np.float64)
+    seq = OracleSequence(m, np.ones(1, np.uint8))
+    res = verify(m, seq, np.array([0, 1, 2]), parent=np.array([-1, 0, 0]))
+    s = np.sqrt(d) / np.sqrt(1.0 + shape.rms_eps * d / c ** 2)
+    np.testing.assert_allclose(res.margin, [s * 0.5, 0.0, s * 1.5], rtol=1e-12, atol=1e-12)
+    assert list(res.greedy) == [17, 9, V - 1]
