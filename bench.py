@@ -9,9 +9,15 @@ probability 0.6, skip masks of 0, 4 and 8 layers drawn from layers 16-31
 lm_head, argmax and accept scan) with commit, followed by a rewind of the
 sequence to its 1024-token context.
 
-Prints one JSON line.  value = accepted tokens/s of the dense verifier
-(sum(accept_len + 1) / sum(step latency)); the skip-4 and skip-8 figures are
-in "by_skip".
+The chain drafts of each mask are a fixed pool of 200 (seeded, drawn whatever
+--steps is); warm-up and timed steps cycle through it.
+
+Prints one compact JSON line.  value = accepted tokens/s of the dense
+verifier over the timed steps (sum(accept_len + 1) / sum(step latency));
+tok_s_at_E divides the expected tokens per step of this draft distribution
+(E[accept_len + 1] = 2.383) by the median latency.  The skip-4 and skip-8
+figures are in "by_skip", other workloads in "workloads" (one summary each);
+--detail-out writes the full records to a file.
 """
 from __future__ import annotations
 
@@ -33,6 +39,12 @@ METRIC = "verify-step latency (µs) & accepted tok/s, 7B-shape k=5, dense vs 4/8
 PEAK_HBM = 8.0e12
 CTX, K_DRAFT, P_ACCEPT = 1024, 5, 0.6
 SKIPS = (0, 4, 8)
+# chain drafts per mask, drawn once whatever --steps is; warm-up and timed
+# steps cycle through them
+DRAFT_POOL = 200
+# expected tokens committed per step with chain drafts of k=5 at p=0.6:
+# E[accept_len + 1] = sum_{j=0..5} 0.6^j
+EXPECTED_TOKENS = sum(P_ACCEPT ** j for j in range(K_DRAFT + 1))
 
 
 def log(msg):
@@ -148,10 +160,13 @@ def run_gpu(args):
         greedy = np.asarray(cur[1:])
         log(f"skip {s}: layers {np.nonzero(mask)[0].tolist()} prefill+greedy {time.time() - t1:.1f}s")
         drafts = [np.concatenate([[root], synth.chain_draft(greedy, shape.vocab, p_accept=P_ACCEPT, stream=i)])
-                  for i in range(args.warmup + args.steps)]
+                  for i in range(DRAFT_POOL)]
+        # accept length of each pool draft: its leading run of greedy tokens
+        pool_accept = np.array([int(np.cumprod(d[1:] == greedy).sum()) for d in drafts])
+
         def timed(n_steps, tag, after_warmup=None):
             for i in range(args.warmup):
-                v.verify(0, drafts[i], commit=True)
+                v.verify(0, drafts[i % DRAFT_POOL], commit=True)
                 v.truncate(0, CTX)
             if after_warmup:
                 after_warmup()
@@ -162,7 +177,7 @@ def run_gpu(args):
             t_start = time.perf_counter()
             for i in range(n_steps):
                 a = time.perf_counter()
-                al, _ = v.verify(0, drafts[args.warmup + i], commit=True)
+                al, _ = v.verify(0, drafts[i % DRAFT_POOL], commit=True)
                 lat[i] = time.perf_counter() - a
                 acc[i] = al
                 v.truncate(0, CTX)
@@ -184,13 +199,18 @@ def run_gpu(args):
         active = shape.n_layers - s
         by = algorithmic_bytes(shape, active, CTX, M)
         med = float(np.median(lat))
+        assert all(int(a) == int(pool_accept[i % DRAFT_POOL]) for i, a in enumerate(acc)), \
+            "accept lengths differ from the drafts' greedy prefixes"
         results[s] = {
             "skipped_layers": np.nonzero(mask)[0].tolist(),
             "latency_us_median": med * 1e6,
             "latency_us_p10": float(np.percentile(lat, 10)) * 1e6,
             "latency_us_p90": float(np.percentile(lat, 90)) * 1e6,
             "accepted_tok_s": float((acc + 1).sum() / lat.sum()),
+            "accepted_tok_s_at_expected": EXPECTED_TOKENS / med,
+            "accepted_tok_s_pool_mean": float((pool_accept + 1).mean()) / med,
             "mean_accept_len": float(acc.mean()),
+            "pool_mean_accept_len": float(pool_accept.mean()),
             "algorithmic_GB": by / 1e9,
             "roofline_latency_us": by / PEAK_HBM * 1e6,
             "roofline_frac": by / PEAK_HBM / med,
@@ -577,56 +597,93 @@ def workload_domains_13b(args):
     return out
 
 
-def cpu_baseline(args, shape, gpu_accept_mean):
-    """The oracle, untouched, on a bounded sample: the 7B verify step with two
-    of the 32 blocks active (KV for the 1024-token context from the oracle's
-    own prefill of those blocks, not timed) and with every block skipped;
-    per-block time x 32 + the block-free time gives the dense step."""
+def _blas_info():
     from threadpoolctl import threadpool_info
+    info = [d for d in threadpool_info() if d.get("user_api") == "blas"] or threadpool_info()
+    threads = max([d.get("num_threads", 1) for d in info] + [1])
+    name = ", ".join(f"{d.get('internal_api', '?')} {d.get('version', '')} ({d.get('threading_layer', '?')})"
+                     for d in info) or "unknown"
+    return int(threads), name
+
+
+def cpu_baseline(args, shape, tokens_per_step):
+    """The oracle, untouched, on bounded samples of the workload's own inputs.
+
+    7B chain k=5 step at a 1024-token context: measured with four of the 32
+    blocks active (their K/V from the oracle's own prefill of the context
+    through those blocks, not timed) and with every block skipped; the dense
+    step is extrapolated as the block-free time plus 32 x the measured
+    per-block time (the oracle's blocks are identical in shape and cost).
+    Tiny fp32 model (4 layers, d 256, mask {2}, 128-token context, chain k=5):
+    the full verify step, timed with one BLAS thread."""
+    from threadpoolctl import threadpool_limits
 
     from oracle import OracleModel, OracleSequence, prefill, verify
 
-    cache = {}
+    def model(sh):
+        cache = {}
 
-    def get(name, layer):
-        if (name, layer) not in cache:
-            cache[(name, layer)] = synth.weight_tensor(shape, name, layer)
-        return cache[(name, layer)]
-    m = OracleModel(shape, get)
-    toks = synth.context_tokens(shape.vocab, CTX + 1)
-    ctx, root = toks[:CTX], int(toks[CTX])
-    two = np.ones(shape.n_layers, np.uint8)
-    two[[0, 1]] = 0
-    seq = OracleSequence(m, two)
-    t = time.time()
-    prefill(m, seq, ctx)
-    log(f"oracle prefill of 2 blocks: {time.time() - t:.1f}s")
-    tokens = np.concatenate([[root], synth.context_tokens(shape.vocab, K_DRAFT, stream=7)])
-    none = np.ones(shape.n_layers, np.uint8)
+        def get(name, layer):
+            if (name, layer) not in cache:
+                cache[(name, layer)] = synth.weight_tensor(sh, name, layer)
+            return cache[(name, layer)]
+        return OracleModel(sh, get)
 
-    def timed(mask, reps):
-        verify(m, seq, tokens, mask=mask)
-        best = []
+    def median_time(fn, reps):
+        fn()
+        t = []
         for _ in range(reps):
             a = time.perf_counter()
-            verify(m, seq, tokens, mask=mask)
-            best.append(time.perf_counter() - a)
-        return float(np.median(best))
-    t2 = timed(two, args.cpu_reps)
-    t0 = timed(none, args.cpu_reps)
-    per_block = (t2 - t0) / 2
-    dense = t0 + shape.n_layers * per_block
-    threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+            fn()
+            t.append(time.perf_counter() - a)
+        return float(np.median(t))
+
+    threads, blas = _blas_info()
+    m = model(shape)
+    toks = synth.context_tokens(shape.vocab, CTX + 1)
+    ctx, root = toks[:CTX], int(toks[CTX])
+    n_act = 4
+    some = np.ones(shape.n_layers, np.uint8)
+    some[:n_act] = 0
+    seq = OracleSequence(m, some)
+    t = time.time()
+    prefill(m, seq, ctx)
+    log(f"oracle prefill through {n_act} blocks: {time.time() - t:.1f}s")
+    tokens = np.concatenate([[root], synth.context_tokens(shape.vocab, K_DRAFT, stream=7)])
+    none = np.ones(shape.n_layers, np.uint8)
+    t_some = median_time(lambda: verify(m, seq, tokens, mask=some), args.cpu_reps)
+    t_none = median_time(lambda: verify(m, seq, tokens, mask=none), args.cpu_reps)
+    per_block = (t_some - t_none) / n_act
+    dense = t_none + shape.n_layers * per_block
+    del m, seq
+
+    tiny = synth.TINY
+    mt = model(tiny)
+    tt = synth.context_tokens(tiny.vocab, 129)
+    tmask = synth.mask_from_layers(tiny.n_layers, [2])
+    tseq = OracleSequence(mt, tmask)
+    prefill(mt, tseq, tt[:128])
+    cur = [int(tt[128])]
+    for _ in range(K_DRAFT):
+        cur.append(int(verify(mt, tseq, np.asarray(cur)).greedy[-1]))
+    tdraft = np.concatenate([cur[:1], synth.chain_draft(np.asarray(cur[1:]), tiny.vocab, n_greedy=3)])
+    with threadpool_limits(limits=1):
+        t_tiny = median_time(lambda: verify(mt, tseq, tdraft), 20)
+    tiny_accept = verify(mt, tseq, tdraft).accept_len
     return {
-        "value": (gpu_accept_mean + 1) / dense,
+        "value": tokens_per_step / dense,
         "unit": "accepted tok/s",
-        "cores": int(threads),
+        "cores": threads,
         "kind": "oracle",
-        "sample": (f"oracle verify of the 7B chain k=5 step at context 1024 with blocks 0-1 active "
-                   f"({t2 * 1e3:.0f} ms) and with all blocks skipped ({t0 * 1e3:.0f} ms), median of "
-                   f"{args.cpu_reps}; dense latency extrapolated as skipped-time + 32 x per-block = "
-                   f"{dense * 1e3:.0f} ms; accepted tokens per step taken from the GPU run's mean"),
+        "sample": (f"numpy fp32 oracle, 7B chain k=5 verify at context 1024, {threads} BLAS threads: measured with "
+                   f"blocks 0-{n_act - 1} active ({t_some * 1e3:.0f} ms) and with every block skipped "
+                   f"({t_none * 1e3:.0f} ms), median of {args.cpu_reps}; dense step extrapolated as "
+                   f"skipped + {shape.n_layers} x per-block = {dense * 1e3:.0f} ms; tokens per step as in the GPU run"),
+        "host_cpus": os.cpu_count(),
+        "blas": blas,
         "latency_ms_extrapolated": dense * 1e3,
+        "tiny_single_thread": {"latency_ms": t_tiny * 1e3, "accept_len": int(tiny_accept),
+                               "accepted_tok_s": (tiny_accept + 1) / t_tiny},
     }
 
 
@@ -643,6 +700,7 @@ def main():
     ap.add_argument("--skips", default="0,4,8", help="skip counts to time; the first is the headline")
     ap.add_argument("--calib-copy", type=float, default=0.0,
                     help="GiB of a plain device copy run first (HBM counter calibration)")
+    ap.add_argument("--detail-out", default="", help="file for the full per-skip, per-mask and workload records")
     args = ap.parse_args()
     args.skips = [int(x) for x in args.skips.split(",")]
     if args.skips[0] != 0 or any(x not in SKIPS for x in args.skips):
@@ -665,7 +723,7 @@ def main():
                 "algorithmic_bytes_per_launch": gb}
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, shape, d0["mean_accept_len"])
+        cpu = cpu_baseline(args, shape, d0["mean_accept_len"] + 1)
     workloads = {}
     runners = {"tree7b": workload_tree_7b, "batch13b": workload_batch_13b, "sweep33b": workload_sweep_33b,
                "decode7b": workload_decode_7b, "search7b": workload_search_7b, "domains13b": workload_domains_13b}
@@ -691,6 +749,33 @@ def main():
         tok_s = w.get("accepted_tok_s")
         log(f"workload {name}: median {w['latency_us_median']:.0f} us"
             + (f", {tok_s:.0f} accepted tok/s" if tok_s is not None else ""))
+    detail = {"by_skip": {str(k): v for k, v in res.items()}, "workloads": workloads, "roofline": roof,
+              "cpu_baseline": cpu}
+    if args.detail_out:
+        with open(args.detail_out, "w") as fh:
+            json.dump(detail, fh, indent=1)
+        log(f"full results written to {args.detail_out}")
+
+    def r(x, n=4):
+        return None if x is None else float(f"{x:.{n}g}")
+
+    by_skip = {str(k): {"skipped": v["skipped_layers"], "us": r(v["latency_us_median"]),
+                        "us_p10_p90": [r(v["latency_us_p10"]), r(v["latency_us_p90"])],
+                        "tok_s": r(v["accepted_tok_s"]), "tok_s_at_E": r(v["accepted_tok_s_at_expected"]),
+                        "frac": r(v["roofline_frac"], 3),
+                        **({"lat_ratio": r(v["latency_ratio_vs_dense"], 3), "byte_ratio": r(v["byte_ratio_vs_dense"], 3)}
+                           if "latency_ratio_vs_dense" in v else {})}
+               for k, v in res.items()}
+    wl = {}
+    for name, w in workloads.items():
+        e = {"us": r(w.get("latency_us_median"))}
+        for key, short in (("roofline_frac", "frac"), ("roofline_frac_median", "frac"), ("accepted_tok_s", "tok_s"),
+                           ("us_per_skipped_layer", "us_per_skip"), ("packed_sweep_ms", "packed_ms"),
+                           ("one_by_one_ms", "one_by_one_ms"), ("speedup", "speedup"),
+                           ("sweep_speedup", "sweep_speedup")):
+            if w.get(key) is not None:
+                e[short] = r(w[key], 3)
+        wl[name] = e
     out = {
         "metric": METRIC,
         "value": d0["accepted_tok_s"],
@@ -705,16 +790,21 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": "7B-shape decoder, chain k=5 (p=0.6), 1024-token paged context, dense mask",
-                   "context": CTX, "k": K_DRAFT, "p_accept": P_ACCEPT, "page_tokens": 16,
-                   "skip_counts": args.skips, "parallelism": "single GPU"},
-        "latency_us_median": d0["latency_us_median"],
-        "step_roofline_frac": d0["roofline_frac"],
-        "roofline": roof,
-        "cpu_baseline": cpu,
-        "by_skip": {str(k): v for k, v in res.items()},
-        "workloads": workloads,
+                   "draft_pool": DRAFT_POOL, "parallelism": "single GPU"},
+        "latency_us_median": r(d0["latency_us_median"]),
+        "step_roofline_frac": r(d0["roofline_frac"], 3),
+        "tok_s_at_expected_accept": r(d0["accepted_tok_s_at_expected"]),
+        "roofline": None if roof is None else {k: (r(v) if isinstance(v, float) else v) for k, v in roof.items()
+                                               if k not in ("launches",)},
+        "cpu_baseline": None if cpu is None else {
+            "value": r(cpu["value"]), "unit": cpu["unit"], "cores": cpu["cores"], "kind": cpu["kind"],
+            "sample": "oracle 7B step extrapolated from a measured 4-block sample (numpy fp32); tiny step 1 thread",
+            "host_cpus": cpu["host_cpus"], "blas": cpu["blas"], "ms": r(cpu["latency_ms_extrapolated"]),
+            "tiny_1thread_ms": r(cpu["tiny_single_thread"]["latency_ms"])},
+        "by_skip": by_skip,
+        "workloads": wl,
     }
-    print(json.dumps(out), flush=True)
+    print(json.dumps(out, separators=(",", ":")), flush=True)
 
 
 if __name__ == "__main__":
