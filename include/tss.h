@@ -201,6 +201,31 @@ int tss_prefill(tss_ctx* ctx, int32_t seq, const int32_t* tokens, int32_t n);
 int tss_verify(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent, int32_t n_nodes,
                const uint8_t* skip_mask, uint32_t flags, int32_t* accept_len, int32_t* next_token);
 
+/* For callers that cannot allocate device memory (serving loops and
+ * harnesses that forbid allocation, which cannot provide tss_create's
+ * workspace for a second context, for example): tss_verify, with the same
+ * arguments, results and errors, but with the step's workspace (activations,
+ * attention partial states, merge counters, K-split partial products,
+ * logits, argmax partials, per-step results) in a static device array of
+ * TSS_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends, instead of the workspace given to tss_create.  It
+ * calls no allocating routine: its launches are direct (never captured into
+ * a graph) and results come back through the context's pinned buffer.
+ *   TSS_ENOSPACE, with a message, when tss_static_workspace_bytes(cfg)
+ *   exceeds TSS_STATIC_SCRATCH_BYTES (larger models use tss_verify).
+ * Every call on a GPU shares that GPU's scratch, which keeps the last call's
+ * contents: calls that overlap on one GPU (from several host threads, or on
+ * streams that run at the same time) race, and the caller must serialise
+ * them.  The merge counters are cleared at the start of every step.
+ * tss_get_logits, tss_get_logits_device, tss_get_greedy and
+ * tss_get_attn_split read the last step's workspace, so after a static call
+ * they are valid only until the next call on that GPU reuses the scratch. */
+#define TSS_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+size_t tss_static_workspace_bytes(const tss_model_cfg* cfg);
+int tss_verify_static(tss_ctx* ctx, int32_t seq, const int32_t* draft_tokens, const int32_t* tree_parent,
+                      int32_t n_nodes, const uint8_t* skip_mask, uint32_t flags, int32_t* accept_len,
+                      int32_t* next_token);
+
 /* Paper: as tss_verify, for several requests, each with its own domain's
  * skip set (Domain-Aware Skip Controller).
  * Verifies several sequences in one step (the same forward as tss_verify, on

@@ -18,7 +18,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libtss.so")
-SOURCES = ["tss_host.cpp", "k_gemm.hip", "k_attn.hip", "k_misc.hip"]
+SOURCES = ["tss_host.cpp", "tss_static.hip", "k_gemm.hip", "k_attn.hip", "k_misc.hip"]
 
 
 def _hipcc():

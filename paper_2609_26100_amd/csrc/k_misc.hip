@@ -23,6 +23,10 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     for (int i = threadIdx.x; i < (int)(sizeof(StepParams) / 4); i += 256) dst[i] = src[i];
     // a step whose blocks are all skipped reports no attention items
     if (threadIdx.x == 0) a.attn_split[2 * kAttnMaxItems] = 0;
+    // the merges' arrival counters start every step at zero (their last
+    // arrivals also reset them; this holds even when another context's step
+    // used the same memory in between)
+    for (int i = threadIdx.x; i < a.n_counters; i += 256) a.counters[i] = 0;
   }
   const float* gain = a.gain[a.sp.row_seq[m]];
   // Each thread takes whole 16-column parts (up to two; d <= 8192): the

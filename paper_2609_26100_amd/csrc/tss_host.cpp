@@ -45,6 +45,7 @@ struct WeightLayout {
 struct WsLayout {
   size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, counters, attn_split, kpart, kcount, logits,
       am_val, am_idx, greedy, total;
+  int n_counters;
 };
 
 // weight element bytes; the KV cache uses the same width (fp16 in the bf16
@@ -137,10 +138,13 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   const size_t slots = attn_slots(c);
   w.part_o = take(slots * kAttnMaxTiles * 16 * c->head_dim * 4);
   w.part_ml = take(slots * kAttnMaxTiles * 16 * 2 * 4);
-  w.counters = take((size_t)c->n_heads * kAttnMaxItems * 4);
+  // arrival counters of the attention merges and of the K-split strips, one
+  // region that every step clears first (embedding kernel)
+  w.counters = take((size_t)c->n_heads * kAttnMaxItems * 4 + (d / 16) * 4);
+  w.kcount = w.counters + (size_t)c->n_heads * kAttnMaxItems * 4;
+  w.n_counters = c->n_heads * kAttnMaxItems + (int)(d / 16);
   w.attn_split = take((2 * kAttnMaxItems + 1) * 4);
   w.kpart = take((size_t)kMaxKSplit * d * Mp * 4);  // K-split partial products of the residual projections
-  w.kcount = take((d / 16) * 4);
   w.logits = take(Mp * v * 4);
   w.am_val = take((v / 16) * Mp * 4);
   w.am_idx = take((v / 16) * Mp * 4);
@@ -174,10 +178,17 @@ struct tss_ctx {
   bool bf16 = false;
   int es = 4, Mp = 16, KC = 16;
   hipStream_t stream = nullptr;
+  int device = 0;                 // device current at creation (the stream's)
   uint8_t* w = nullptr;
-  uint8_t* ws = nullptr;
+  uint8_t* ws = nullptr;          // workspace of the next step (the caller's, or the static scratch)
   WeightLayout wl;
   WsLayout wsl{};
+  int Mp_own = 16;
+  uint8_t* ws_own = nullptr;      // the caller's workspace and its layout
+  WsLayout wsl_own{};
+  const uint8_t* out_ws = nullptr;  // workspace and layout of the last step (logits, greedy, split report)
+  WsLayout out_wsl{};
+  bool direct_only = false;       // set while a step must not be captured (static scratch)
   // KV pool
   uint8_t* kv = nullptr;
   KvLayout kvl;
@@ -399,11 +410,18 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
   c->Mp = round16(row_cap(cfg));
   c->stream = (hipStream_t)hip_stream;
   c->w = (uint8_t*)dev_weights;
-  c->ws = (uint8_t*)dev_workspace;
+  c->ws = c->ws_own = (uint8_t*)dev_workspace;
+  c->out_ws = c->ws;
   c->wl = weight_layout(cfg);
-  c->wsl = ws_layout(cfg);
-  const char* where = "pinned step parameters";
-  hipError_t e = hipHostMalloc((void**)&c->sp_host, sizeof(StepParams), hipHostMallocDefault);
+  c->wsl = c->wsl_own = c->out_wsl = ws_layout(cfg);
+  c->Mp_own = c->Mp;
+  c->step.mask.reserve((size_t)kMaxSegs * cfg->n_layers);
+  const char* where = "current device";
+  hipError_t e = hipGetDevice(&c->device);
+  if (e == hipSuccess) {
+    where = "pinned step parameters";
+    e = hipHostMalloc((void**)&c->sp_host, sizeof(StepParams), hipHostMallocDefault);
+  }
   auto step = [&](const char* w, hipError_t r) {
     if (e == hipSuccess) {
       where = w;
@@ -415,10 +433,7 @@ int tss_create(const tss_model_cfg* cfg, void* hip_stream, void* dev_weights, si
          hipHostMalloc((void**)&c->res_host, kMaxSegs * sizeof(Result), hipHostMallocMapped | hipHostMallocCoherent));
   if (e == hipSuccess) step("mapped result address", hipHostGetDevicePointer((void**)&c->res_dev_map, c->res_host, 0));
   if (e == hipSuccess)
-    step("attention counters",
-         hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)cfg->n_heads * kAttnMaxItems * 4, c->stream));
-  if (e == hipSuccess)
-    step("K-split counters", hipMemsetAsync(c->ws + c->wsl.kcount, 0, (size_t)(cfg->d_model / 16) * 4, c->stream));
+    step("merge counters", hipMemsetAsync(c->ws + c->wsl.counters, 0, (size_t)c->wsl.n_counters * 4, c->stream));
   if (e == hipSuccess) step("stream sync", hipStreamSynchronize(c->stream));
   if (e == hipSuccess) step("attention LDS attribute", init_kernel_attributes());
   if (e == hipSuccess) step("projection LDS attribute", init_gemm_attributes());
@@ -966,9 +981,13 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
   return TSS_OK;
 }
 
-// Waits for the step and collects the profiled launch's event times.
+// Waits for the step and collects the profiled launch's event times.  The
+// step's outputs (logits, greedy tokens, split report) are in the workspace
+// it ran on, whether it was enqueued now or replayed from a captured graph.
 int finish_step(tss_ctx* c) {
   HIPCHK(hipStreamSynchronize(c->stream), "step");
+  c->out_ws = c->ws;
+  c->out_wsl = c->wsl;
   if (c->prof_armed) {
     float ms = 0.f;
     HIPCHK(hipEventElapsedTime(&ms, c->ev0, c->ev1), "event timing");
@@ -1007,6 +1026,8 @@ EmbedArgs embed_args(tss_ctx* c, int start_layer, const float* src_h) {
   a.d = cf.d_model;
   a.M = sp.M;
   a.attn_split = (int32_t*)(c->ws + c->wsl.attn_split);
+  a.counters = (int32_t*)(c->ws + c->wsl.counters);
+  a.n_counters = c->wsl.n_counters;
   return a;
 }
 
@@ -1169,7 +1190,7 @@ int verify_batch(tss_ctx* c, int32_t n_seqs, const int32_t* seq_ids, const int32
   sp.seq_row0[n_seqs] = M;
   // event timing of one launch needs direct launches (events recorded inside a
   // captured graph cannot be timed)
-  const bool graph = c->launch_mode == TSS_LAUNCH_GRAPH && c->prof_kind < 0;
+  const bool graph = c->launch_mode == TSS_LAUNCH_GRAPH && c->prof_kind < 0 && !c->direct_only;
   const int r = graph ? run_verify_graph(c) : run_step(c, true);
   if (r) return r;
   c->last_M = M;
@@ -1389,6 +1410,13 @@ int tss_verify(tss_ctx* c, int32_t seq, const int32_t* draft_tokens, const int32
   return verify_batch(c, 1, &seq, offs, draft_tokens, tree_parent, skip_mask, flags, accept_len, next_token);
 }
 
+size_t tss_static_workspace_bytes(const tss_model_cfg* cfg) {
+  if (!cfg_ok(cfg)) return 0;
+  tss_model_cfg one = *cfg;
+  one.max_batch = 1;
+  return ws_layout(&one).total;
+}
+
 int tss_verify_batch(tss_ctx* c, int32_t n_seqs, const int32_t* seq_ids, const int32_t* node_offsets,
                      const int32_t* draft_tokens, const int32_t* tree_parents, const uint8_t* skip_masks,
                      uint32_t flags, int32_t* accept_len, int32_t* next_token) {
@@ -1402,7 +1430,8 @@ int tss_get_logits(tss_ctx* c, float* host_dst, int32_t n_nodes) {
   if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
   if (n_nodes < 1 || n_nodes > c->last_M) return fail(c, TSS_EINVAL, "n_nodes exceeds the last verify's nodes");
   HIPCHK(hipStreamSynchronize(c->stream), "sync");
-  HIPCHK(hipMemcpy(host_dst, c->ws + c->wsl.logits, (size_t)n_nodes * c->cfg.vocab * 4, hipMemcpyDeviceToHost),
+  HIPCHK(hipMemcpy(host_dst, c->out_ws + c->out_wsl.logits, (size_t)n_nodes * c->cfg.vocab * 4,
+                   hipMemcpyDeviceToHost),
          "logits copy");
   return TSS_OK;
 }
@@ -1421,7 +1450,8 @@ int tss_get_logits_device(tss_ctx* c, float* dev_dst, int32_t n_nodes) {
   if (!c || !dev_dst) return TSS_EINVAL;
   if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
   if (n_nodes < 1 || n_nodes > c->last_M) return fail(c, TSS_EINVAL, "n_nodes exceeds the last verify's nodes");
-  HIPCHK(hipMemcpyAsync(dev_dst, c->ws + c->wsl.logits, (size_t)n_nodes * c->cfg.vocab * 4, hipMemcpyDeviceToDevice,
+  HIPCHK(hipMemcpyAsync(dev_dst, c->out_ws + c->out_wsl.logits, (size_t)n_nodes * c->cfg.vocab * 4,
+                        hipMemcpyDeviceToDevice,
                         c->stream),
          "logits copy");
   return TSS_OK;
@@ -1432,7 +1462,7 @@ int tss_get_attn_split(tss_ctx* c, int32_t* n_items, int32_t* groups, int32_t* r
   if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
   int32_t rep[2 * kAttnMaxItems + 1];
   HIPCHK(hipStreamSynchronize(c->stream), "sync");
-  HIPCHK(hipMemcpy(rep, c->ws + c->wsl.attn_split, sizeof(rep), hipMemcpyDeviceToHost), "split copy");
+  HIPCHK(hipMemcpy(rep, c->out_ws + c->out_wsl.attn_split, sizeof(rep), hipMemcpyDeviceToHost), "split copy");
   const int n = std::max(0, std::min(rep[2 * kAttnMaxItems], kAttnMaxItems));
   *n_items = n;
   for (int i = 0; i < n; ++i) {
@@ -1475,8 +1505,51 @@ int tss_get_greedy(tss_ctx* c, int32_t* host_dst, int32_t n_nodes) {
   if (c->poisoned) return fail(c, TSS_ESTATE, "context poisoned by an earlier HIP error");
   if (n_nodes < 1 || n_nodes > c->last_M) return fail(c, TSS_EINVAL, "n_nodes exceeds the last verify's nodes");
   HIPCHK(hipStreamSynchronize(c->stream), "sync");
-  HIPCHK(hipMemcpy(host_dst, c->ws + c->wsl.greedy, (size_t)n_nodes * 4, hipMemcpyDeviceToHost), "greedy copy");
+  HIPCHK(hipMemcpy(host_dst, c->out_ws + c->out_wsl.greedy, (size_t)n_nodes * 4, hipMemcpyDeviceToHost),
+         "greedy copy");
   return TSS_OK;
 }
 
 }  // extern "C"
+
+// Internal interface of tss_verify_static (tss_static.hip, which holds the
+// static scratch).
+namespace tss {
+
+int static_prepare(tss_ctx* c, int32_t seq, int* device) {
+  const int r = check_ready(c, seq);
+  if (r) return r;
+  const size_t need = tss_static_workspace_bytes(&c->cfg);
+  if (need > (size_t)TSS_STATIC_SCRATCH_BYTES)
+    return fail(c, TSS_ENOSPACE,
+                "this model's single-sequence workspace (" + std::to_string(need) +
+                    " bytes) exceeds the static scratch of " + std::to_string((size_t)TSS_STATIC_SCRATCH_BYTES) +
+                    " bytes; use tss_verify with the context's workspace");
+  *device = c->device;
+  return TSS_OK;
+}
+
+int static_hip_fail(tss_ctx* c, hipError_t e, const char* where) { return hip_fail(c, e, where); }
+
+int verify_in_workspace(tss_ctx* c, uint8_t* base, int32_t seq, const int32_t* tokens, const int32_t* parent,
+                        int32_t n_nodes, const uint8_t* mask, uint32_t flags, int32_t* accept_len,
+                        int32_t* next_token) {
+  tss_model_cfg one = c->cfg;
+  one.max_batch = 1;
+  // the step runs on `base` in the single-sequence layout, with direct
+  // launches (a captured step would keep the addresses); the context's own
+  // workspace is restored afterwards
+  c->ws = base;
+  c->wsl = ws_layout(&one);
+  c->Mp = round16(row_cap(&one));
+  c->direct_only = true;
+  const int32_t offs[2] = {0, n_nodes};
+  const int r = verify_batch(c, 1, &seq, offs, tokens, parent, mask, flags, accept_len, next_token);
+  c->ws = c->ws_own;
+  c->wsl = c->wsl_own;
+  c->Mp = c->Mp_own;
+  c->direct_only = false;
+  return r;
+}
+
+}  // namespace tss

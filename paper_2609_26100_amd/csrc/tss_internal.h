@@ -41,6 +41,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+struct tss_ctx;
+
 namespace tss {
 
 constexpr int kPage = 16;          // tokens per KV page
@@ -256,6 +258,8 @@ struct EmbedArgs {
   int ss_stride;
   int d, M;
   int32_t* attn_split;     // the attention split report (AttnArgs::split_out): its item count is cleared
+  int32_t* counters;       // arrival counters of the step's merges (attention, K split), cleared here
+  int n_counters;
 };
 
 struct AcceptArgs {
@@ -311,6 +315,18 @@ const void* embed_kernel(bool bf16);  // kernel symbol, for updating a captured 
 hipError_t init_kernel_attributes();  // attention
 hipError_t init_gemm_attributes();
 hipError_t launch_rope_table(float2* tab, int max_pos, int head_dim, float base, hipStream_t s);
+
+// Host runtime pieces of tss_verify_static (tss_static.hip holds the static
+// scratch): the checks before any device work (sequence state, the model's
+// single-sequence workspace against the scratch size; the context's device),
+// the error of a failed HIP call, and a single-sequence verify whose step
+// workspace is `base` (direct launches; the context's own workspace is
+// restored afterwards).
+int static_prepare(tss_ctx* c, int32_t seq, int* device);
+int static_hip_fail(tss_ctx* c, hipError_t e, const char* where);
+int verify_in_workspace(tss_ctx* c, uint8_t* base, int32_t seq, const int32_t* tokens, const int32_t* parent,
+                        int32_t n_nodes, const uint8_t* mask, uint32_t flags, int32_t* accept_len,
+                        int32_t* next_token);
 
 // 16-column tiles per workgroup of a projection launch.  A workgroup streams
 // its tiles over all of K, so every workgroup reads all of the step's

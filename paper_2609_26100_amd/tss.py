@@ -28,8 +28,11 @@ EXPORTS = (
     "tss_load_weights", "tss_kv_alloc", "tss_set_skip_mask", "tss_prefill", "tss_verify", "tss_get_logits",
     "tss_verify_batch", "tss_verify_sweep", "tss_sweep_prefix_bytes", "tss_get_greedy", "tss_get_path", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
     "tss_tree_meta", "tss_set_launch_mode", "tss_profile_kernel", "tss_profile_read", "tss_last_error", "tss_status_string",
-    "tss_destroy", "tss_get_logits_device", "tss_get_attn_split", "tss_check_kv",
+    "tss_destroy", "tss_get_logits_device", "tss_get_attn_split", "tss_check_kv", "tss_verify_static",
+    "tss_static_workspace_bytes",
 )
+
+TSS_STATIC_SCRATCH_BYTES = 64 << 20
 
 
 class tss_model_cfg(ctypes.Structure):
@@ -78,6 +81,9 @@ def lib():
             "tss_get_logits_device": (ctypes.c_int, [P, P, I32]),
             "tss_get_attn_split": (ctypes.c_int, [P, ctypes.POINTER(I32), P, P]),
             "tss_check_kv": (ctypes.c_int, [P]),
+            "tss_verify_static": (ctypes.c_int, [P, I32, P, P, I32, P, U32, ctypes.POINTER(I32),
+                                                 ctypes.POINTER(I32)]),
+            "tss_static_workspace_bytes": (SZ, [CFG]),
             "tss_get_path": (ctypes.c_int, [P, I32, P, ctypes.POINTER(I32)]),
             "tss_seq_length": (ctypes.c_int, [P, I32, ctypes.POINTER(I32)]),
             "tss_seq_truncate": (ctypes.c_int, [P, I32, I32]),
@@ -175,6 +181,22 @@ def tss_verify(ctx, seq, draft_tokens, tree_parent=None, skip_mask=None, flags=0
     _check(lib().tss_verify(ctx, seq, _ptr(t), _ptr(p), len(t), _ptr(m), flags, ctypes.byref(al), ctypes.byref(nt)),
            ctx, "tss_verify")
     return al.value, nt.value
+
+
+def tss_verify_static(ctx, seq, draft_tokens, tree_parent=None, skip_mask=None, flags=0):
+    """tss_verify with the step's workspace in the library's static device scratch (allocates nothing).
+    Returns (accept_len, next_token)."""
+    t = np.ascontiguousarray(draft_tokens, dtype=np.int32)
+    p = None if tree_parent is None else np.ascontiguousarray(tree_parent, dtype=np.int32)
+    m = None if skip_mask is None else np.ascontiguousarray(skip_mask, dtype=np.uint8)
+    al, nt = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().tss_verify_static(ctx, seq, _ptr(t), _ptr(p), len(t), _ptr(m), flags, ctypes.byref(al),
+                                   ctypes.byref(nt)), ctx, "tss_verify_static")
+    return al.value, nt.value
+
+
+def tss_static_workspace_bytes(cfg) -> int:
+    return lib().tss_static_workspace_bytes(ctypes.byref(cfg))
 
 
 def tss_verify_batch(ctx, seq_ids, draft_tokens, node_offsets, tree_parents=None, skip_masks=None, flags=0):

@@ -147,3 +147,22 @@ def test_sweep_prefix_bytes():
     assert abi.tss_sweep_prefix_bytes(cfg, 33) == 32 * 33 * 4096 * 4
     assert abi.tss_sweep_prefix_bytes(cfg, 0) == 0
     assert abi.tss_sweep_prefix_bytes(cfg, 65) == 0
+
+
+def test_static_scratch_sizes():
+    """tss_verify_static serves every workload shape's single-sequence steps
+    (up to 64 nodes) from the 64 MiB static scratch; the size query follows
+    the single-sequence layout whatever max_batch is, and a model with a
+    d 8192, 64000-token vocabulary is reported as not fitting (its partial
+    states, activations and logits exceed the scratch)."""
+    for shape in (synth.TINY, synth.LLAMA_7B, synth.LLAMA_13B, synth.LLAMA_33B):
+        one = abi.tss_static_workspace_bytes(abi.make_cfg(shape, 64, 1))
+        assert 0 < one <= abi.TSS_STATIC_SCRATCH_BYTES
+        assert abi.tss_static_workspace_bytes(abi.make_cfg(shape, 64, 8)) == one
+        assert abi.tss_workspace_bytes(abi.make_cfg(shape, 64, 1)) == one
+    big = synth.ModelShape("d8192-v64000", 90, n_layers=1, d_model=8192, n_heads=64, head_dim=128, ffn_dim=64,
+                           vocab=64000)
+    assert abi.tss_static_workspace_bytes(abi.make_cfg(big, 64, 1)) > abi.TSS_STATIC_SCRATCH_BYTES
+    bad = abi.make_cfg(synth.TINY)
+    bad.head_dim = 96
+    assert abi.tss_static_workspace_bytes(bad) == 0
