@@ -513,11 +513,8 @@ def workload_search_7b(args):
         items.append((i, d.astype(np.int32), None))
     quality = SweepQuality(v, items)
     cost = MeasuredCost(v, items[0], reps=5)
-    lines = []
     res = breadth_search(shape.n_layers, 4, quality, cost, eps_A=0.05, eps_M=1.0, tau_A=0.0, tau_M=0.0,
-                         relative=True, log=lines.append)
-    for ln in lines:
-        log("search: " + ln)
+                         relative=True, log=lambda ln: log("search: " + ln))
     # sweep throughput: 64 masks of 1-4 layers from 16-31, packed vs one verify per mask
     rng = np.random.default_rng(5)
     masks = np.stack([synth.random_skip_mask(shape.n_layers, 16, 31, int(rng.integers(1, 5)), stream=900 + j)

@@ -96,10 +96,12 @@ enum tss_kernel {
  *   d_model <= 8192 (<= 4096 for TSS_F32);
  * One step carries at most min(max_nodes * max_batch, 128) rows (64 for
  * TSS_F32): the nodes of all its sequences.
- *   dtype TSS_BF16 (bf16 weights; fp16 KV cache and attention operands; fp32
- *   activations fed to the projections as bf16 hi/lo pairs; fp32
- *   accumulation, residual stream, softmax and logits) or TSS_F32 (everything
- *   fp32).
+ *   dtype TSS_BF16 (bf16 weights, held as fp16: exact for magnitudes
+ *   2^-17 .. 65504, smaller ones within 2^-25, larger ones refused by
+ *   tss_load_weights with TSS_EINVAL; fp16 KV cache, attention operands and
+ *   projection inputs, i.e. fp16 MFMAs as in the paper's fp16 runs; fp32
+ *   accumulation, residual stream, softmax and logits) or TSS_F32
+ *   (everything fp32).
  * The KV page size is fixed at 16 tokens. */
 typedef struct {
   int32_t n_layers;
@@ -126,6 +128,17 @@ int tss_cfg_check(const tss_model_cfg* cfg);
 size_t tss_weights_bytes(const tss_model_cfg* cfg);
 size_t tss_workspace_bytes(const tss_model_cfg* cfg);
 size_t tss_kv_bytes(const tss_model_cfg* cfg, int32_t n_seqs, int32_t max_tokens_per_seq);
+
+/* The conversion tss_load_weights applies to TSS_BF16 weights, on the host:
+ * src[n] bf16 bit patterns to dst[n] fp16 bit patterns of the same value,
+ * round to nearest even (exact for magnitudes 2^-14 .. 65280; below that the
+ * nearest multiple of 2^-24; infinities and NaNs map across, NaNs quiet).
+ * Returns the number of finite values of magnitude >= 65536, which become
+ * infinities here and make tss_load_weights refuse the tensor; -1 for n < 0
+ * or a NULL buffer with n > 0.  Host memory only; no GPU call.  Paper:
+ * Appendix, Experimental Setup / Models and Hardware and Software (the
+ * target's weights are held in float16). */
+int64_t tss_bf16_to_f16(const uint16_t* src, uint16_t* dst, int64_t n);
 
 /* Creates a context bound to hip_stream (a hipStream_t; NULL = the null
  * stream), a packed-weight buffer of tss_weights_bytes() and a workspace of

@@ -501,8 +501,8 @@ static hipError_t attn_attr_hd() {
 // Raises the LDS limit of the attention kernels (more than 64 KiB); done once
 // at context creation so that no attribute call falls inside a captured step.
 hipError_t init_kernel_attributes() {
-  hipError_t e = attn_attr_hd<_Float16, __bf16, 128>();
-  if (e == hipSuccess) e = attn_attr_hd<_Float16, __bf16, 64>();
+  hipError_t e = attn_attr_hd<_Float16, _Float16, 128>();
+  if (e == hipSuccess) e = attn_attr_hd<_Float16, _Float16, 64>();
   if (e == hipSuccess) e = attn_attr_hd<float, float, 128>();
   if (e == hipSuccess) e = attn_attr_hd<float, float, 64>();
   return e;
@@ -526,8 +526,8 @@ static hipError_t attn_hd(int tiles, int n_seq, const AttnArgs& a, hipStream_t s
 hipError_t launch_attn(bool bf16, int head_dim, int max_tiles, int n_seq, const AttnArgs& a, hipStream_t s) {
   if (max_tiles < 1 || max_tiles > 4 || n_seq < 1 || n_seq > kAttnMaxItems) return hipErrorInvalidValue;
   if (bf16)
-    return head_dim == 128 ? attn_hd<_Float16, __bf16, 128>(max_tiles, n_seq, a, s)
-                           : attn_hd<_Float16, __bf16, 64>(max_tiles, n_seq, a, s);
+    return head_dim == 128 ? attn_hd<_Float16, _Float16, 128>(max_tiles, n_seq, a, s)
+                           : attn_hd<_Float16, _Float16, 64>(max_tiles, n_seq, a, s);
   return head_dim == 128 ? attn_hd<float, float, 128>(max_tiles, n_seq, a, s)
                          : attn_hd<float, float, 64>(max_tiles, n_seq, a, s);
 }

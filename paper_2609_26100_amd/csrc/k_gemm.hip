@@ -15,10 +15,8 @@
 //     and the partial sums meet in LDS in a fixed order (no atomics: results
 //     are bit-reproducible).
 //   * Rows are padded to 16 for the MFMA; padded rows load nothing.
-//   * bf16: W in bf16; the fp32 activations arrive as hi and lo bf16 planes
-//     and each W tile meets both (two v_mfma_f32_16x16x32_bf16), so the
-//     product keeps about 16 significant bits of the activation at no extra
-//     HBM traffic (MFMA is idle at these row counts).  f32: four
+//   * fp16 (the bf16-weight mode): W and the activations in fp16, one
+//     v_mfma_f32_16x16x32_f16 per tile and chunk.  f32: four
 //     v_mfma_f32_16x16x4_f32 per 16-byte chunk.
 // Epilogues fuse the element-wise work around each projection:
 //   EPI_QKV     RMSNorm row scale, rotate-half RoPE at each node's position,
@@ -31,16 +29,16 @@
 
 namespace tss {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <typename T>
 __device__ __forceinline__ f32x4 mfma_chunk(const uint4& a, const uint4& b, f32x4 c);
 
 template <>
-__device__ __forceinline__ f32x4 mfma_chunk<__bf16>(const uint4& a, const uint4& b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
-                                                 0, 0, 0);
+__device__ __forceinline__ f32x4 mfma_chunk<_Float16>(const uint4& a, const uint4& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                0, 0);
 }
 
 template <>
@@ -110,7 +108,10 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
   constexpr int KL = KC / 4;           // K elements per lane per tile
   constexpr int S = Mode<T>::planes;
-  constexpr int D = Depth<MT, NT, S, EPI>::v;
+  // ring depths were tuned with 16-bit activations in two planes; the one
+  // fp16 plane keeps the same depths (its slots need half the activation
+  // registers)
+  constexpr int D = Depth<MT, NT, sizeof(T) == 2 ? 2 : S, EPI>::v;
   using KV = typename Mode<T>::KV;
   constexpr int ROWS = MT * 16;
   constexpr int COLS = NT * 16;
@@ -492,14 +493,14 @@ static hipError_t gemm_attr_rows() {
 }
 
 hipError_t init_gemm_attributes() {
-  hipError_t e = gemm_attr_rows<__bf16, 1>();
-  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 2>();
-  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 3>();
-  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 4>();
-  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 5>();
-  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 6>();
-  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 7>();
-  if (e == hipSuccess) e = gemm_attr_rows<__bf16, 8>();
+  hipError_t e = gemm_attr_rows<_Float16, 1>();
+  if (e == hipSuccess) e = gemm_attr_rows<_Float16, 2>();
+  if (e == hipSuccess) e = gemm_attr_rows<_Float16, 3>();
+  if (e == hipSuccess) e = gemm_attr_rows<_Float16, 4>();
+  if (e == hipSuccess) e = gemm_attr_rows<_Float16, 5>();
+  if (e == hipSuccess) e = gemm_attr_rows<_Float16, 6>();
+  if (e == hipSuccess) e = gemm_attr_rows<_Float16, 7>();
+  if (e == hipSuccess) e = gemm_attr_rows<_Float16, 8>();
   if (e == hipSuccess) e = gemm_attr_rows<float, 1>();
   if (e == hipSuccess) e = gemm_attr_rows<float, 2>();
   if (e == hipSuccess) e = gemm_attr_rows<float, 3>();
@@ -560,14 +561,14 @@ hipError_t launch_gemm(bool bf16, int epi, int mt, int nt, const GemmArgs& a, hi
     return hipErrorInvalidValue;
   if (bf16) {
     switch (mt) {
-      case 1: return launch_rows<__bf16, 1>(epi, nt, a, s);
-      case 2: return launch_rows<__bf16, 2>(epi, nt, a, s);
-      case 3: return launch_rows<__bf16, 3>(epi, nt, a, s);
-      case 4: return launch_rows<__bf16, 4>(epi, nt, a, s);
-      case 5: return launch_rows<__bf16, 5>(epi, nt, a, s);
-      case 6: return launch_rows<__bf16, 6>(epi, nt, a, s);
-      case 7: return launch_rows<__bf16, 7>(epi, nt, a, s);
-      case 8: return launch_rows<__bf16, 8>(epi, nt, a, s);
+      case 1: return launch_rows<_Float16, 1>(epi, nt, a, s);
+      case 2: return launch_rows<_Float16, 2>(epi, nt, a, s);
+      case 3: return launch_rows<_Float16, 3>(epi, nt, a, s);
+      case 4: return launch_rows<_Float16, 4>(epi, nt, a, s);
+      case 5: return launch_rows<_Float16, 5>(epi, nt, a, s);
+      case 6: return launch_rows<_Float16, 6>(epi, nt, a, s);
+      case 7: return launch_rows<_Float16, 7>(epi, nt, a, s);
+      case 8: return launch_rows<_Float16, 8>(epi, nt, a, s);
       default: return hipErrorInvalidValue;
     }
   }

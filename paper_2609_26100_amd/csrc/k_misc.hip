@@ -236,12 +236,12 @@ __global__ void k_rope_table(float2* tab, int max_pos, int head_dim, float base)
 }
 
 const void* embed_kernel(bool bf16) {
-  return bf16 ? (const void*)k_embed<__bf16> : (const void*)k_embed<float>;
+  return bf16 ? (const void*)k_embed<_Float16> : (const void*)k_embed<float>;
 }
 
 hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s) {
   if (bf16)
-    TSS_LAUNCH(k_embed<__bf16>, dim3(a.M), dim3(256), 0, s, a);
+    TSS_LAUNCH(k_embed<_Float16>, dim3(a.M), dim3(256), 0, s, a);
   else
     TSS_LAUNCH(k_embed<float>, dim3(a.M), dim3(256), 0, s, a);
   return hipGetLastError();

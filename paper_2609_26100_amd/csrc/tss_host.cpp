@@ -12,6 +12,7 @@
 #include "tss_internal.h"
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -51,8 +52,73 @@ struct WsLayout {
 // weight element bytes; the KV cache uses the same width (fp16 in the bf16
 // mode, fp32 in the f32 mode)
 int elem_size(const tss_model_cfg* c) { return c->dtype == TSS_BF16 ? 2 : 4; }
-// activation planes: two bf16 planes (hi, lo) in the bf16 mode, one fp32 plane otherwise
-int act_planes(const tss_model_cfg* c) { return c->dtype == TSS_BF16 ? 2 : 1; }
+// activation planes: one fp16 plane in the bf16-weight mode, one fp32 plane
+// otherwise
+int act_planes(const tss_model_cfg*) { return 1; }
+
+// A bf16 bit pattern as the fp16 bit pattern of the same value, rounded to
+// nearest even.  bf16 keeps 7 fraction bits and fp16 10, so every normal fp16
+// value is exact: exponents 2^-14 .. 2^15 map across unchanged.  Below 2^-14
+// the value (1.m * 2^(e-127), as an integer (128 + m) in units of 2^(e-134))
+// becomes a multiple of fp16's subnormal unit 2^-24 with a rounded right
+// shift.  Finite values from 65536 up (no fp16 value of the same magnitude)
+// set *over and become infinity; infinities and NaNs (kept quiet) map across.
+uint16_t bf16_bits_to_f16(uint16_t b, bool* over) {
+  const uint16_t sign = b & 0x8000u;
+  const uint32_t e = (b >> 7) & 0xffu, m = b & 0x7fu;
+  if (e == 0xff) return sign | 0x7c00u | (m ? 0x200u | (m << 3) : 0u);
+  if (e >= 143) {
+    *over = true;
+    return sign | 0x7c00u;
+  }
+  if (e >= 113) return sign | (uint16_t)(((e - 112) << 10) | (m << 3));
+  if (e == 0) return sign;  // bf16 subnormals lie below 2^-126
+  const uint32_t v = 128u + m;  // value = v * 2^(e - 134), unit 2^-24 for e = 110
+  if (e >= 110) return sign | (uint16_t)(v << (e - 110));
+  const uint32_t k = 110 - e;
+  if (k > 9) return sign;  // below half of 2^-24
+  uint32_t q = v >> k;
+  const uint32_t r = v & ((1u << k) - 1), half = 1u << (k - 1);
+  q += (r > half || (r == half && (q & 1u))) ? 1u : 0u;
+  return sign | (uint16_t)q;
+}
+
+// The whole map as a table (128 KiB, built once): weight uploads convert
+// through it at about one load per element.
+const uint16_t* f16_table() {
+  static const std::vector<uint16_t> tab = [] {
+    std::vector<uint16_t> t(65536);
+    bool over = false;
+    for (uint32_t b = 0; b < 65536; ++b) t[b] = bf16_bits_to_f16((uint16_t)b, &over);
+    return t;
+  }();
+  return tab.data();
+}
+
+// Finite with magnitude >= 65536 (bf16 0x4780): no fp16 value is that large.
+bool bf16_out_of_f16_range(uint16_t b) {
+  const uint16_t a = b & 0x7fffu;
+  return a >= 0x4780u && a < 0x7f80u;
+}
+
+// Copies n_bytes of 16-bit weights, converting bf16 to fp16 when to_f16 is
+// set; clears *ok on a finite value beyond fp16's range.
+void copy_weights(uint8_t* dst, const uint8_t* src, size_t n_bytes, bool to_f16, std::atomic<bool>* ok) {
+  if (!to_f16) {
+    std::memcpy(dst, src, n_bytes);
+    return;
+  }
+  const uint16_t* tab = f16_table();
+  bool over = false;
+  for (size_t i = 0; i < n_bytes; i += 2) {
+    uint16_t b;
+    std::memcpy(&b, src + i, 2);
+    over |= bf16_out_of_f16_range(b);
+    const uint16_t h = tab[b];
+    std::memcpy(dst + i, &h, 2);
+  }
+  if (over) ok->store(false);
+}
 int round16(int x) { return (x + 15) & ~15; }
 // rows one step can carry: the nodes of every sequence of a batch (the GEMMs
 // take up to 8 sixteen-row tiles in the bf16 mode, 4 in the f32 mode)
@@ -313,7 +379,8 @@ int qkv_src_row(int n_in_section, int head_dim) {
 // tiles.  Output tile (r, c) for row tile r and K chunk c is written to
 // dst + (r * nkc + c) * tile_stride; row_map gives the source row of packed row n.
 template <typename RowMap>
-void pack_tiles(uint8_t* dst, const uint8_t* src, int rows, int K, int es, size_t tile_stride, RowMap row_map) {
+void pack_tiles(uint8_t* dst, const uint8_t* src, int rows, int K, int es, size_t tile_stride, RowMap row_map,
+                bool to_f16, std::atomic<bool>* ok) {
   const int KC = 64 / es, KL = KC / 4;
   const int nkc = K / KC;
   const int row_tiles = rows / 16;
@@ -325,7 +392,7 @@ void pack_tiles(uint8_t* dst, const uint8_t* src, int rows, int K, int es, size_
       for (int c = 0; c < nkc; ++c) {
         uint8_t* t = dst + ((size_t)r * nkc + c) * tile_stride;
         for (int l = 0; l < 64; ++l)
-          std::memcpy(t + l * 16, srow[l & 15] + ((size_t)c * KC + (l >> 4) * KL) * es, 16);
+          copy_weights(t + l * 16, srow[l & 15] + ((size_t)c * KC + (l >> 4) * KL) * es, 16, to_f16, ok);
       }
     }
   };
@@ -355,6 +422,17 @@ extern "C" {
 int tss_cfg_check(const tss_model_cfg* cfg) { return cfg_ok(cfg) ? TSS_OK : TSS_EINVAL; }
 
 size_t tss_weights_bytes(const tss_model_cfg* cfg) { return cfg_ok(cfg) ? weight_layout(cfg).total : 0; }
+
+int64_t tss_bf16_to_f16(const uint16_t* src, uint16_t* dst, int64_t n) {
+  if (n < 0 || (n > 0 && (!src || !dst))) return -1;
+  const uint16_t* tab = f16_table();
+  int64_t over = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    over += bf16_out_of_f16_range(src[i]) ? 1 : 0;
+    dst[i] = tab[src[i]];
+  }
+  return over;
+}
 
 size_t tss_workspace_bytes(const tss_model_cfg* cfg) { return cfg_ok(cfg) ? ws_layout(cfg).total : 0; }
 
@@ -491,14 +569,19 @@ int tss_load_weights(tss_ctx* c, int32_t first, int32_t count, const void* const
     return hipEventSynchronize(c->stage_ev[i]);
   };
   auto stage_done = [&](int used) { return hipEventRecord(c->stage_ev[used], c->stream); };
-  auto raw = [&](size_t off, const void* src, size_t bytes) -> hipError_t {
+  // bf16 weights are stored as fp16 (the MFMA operand type of the mode)
+  const bool to_f16 = c->bf16;
+  std::atomic<bool> in_range{true};
+  // raw copies: the embedding (16-bit, converted like the packed weights) and
+  // the fp32 norm gains (never converted)
+  auto raw = [&](size_t off, const void* src, size_t bytes, bool convert) -> hipError_t {
     for (size_t done = 0; done < bytes; done += kStageBytes) {
       const size_t n = std::min(kStageBytes, bytes - done);
       const int used = c->stage_cur;
       uint8_t* b;
       hipError_t e = next_stage(&b);
       if (e != hipSuccess) return e;
-      std::memcpy(b, (const uint8_t*)src + done, n);
+      copy_weights(b, (const uint8_t*)src + done, n, convert && to_f16, &in_range);
       e = hipMemcpyAsync(c->w + off + done, b, n, hipMemcpyHostToDevice, c->stream);
       if (e == hipSuccess) e = stage_done(used);
       if (e != hipSuccess) return e;
@@ -516,7 +599,7 @@ int tss_load_weights(tss_ctx* c, int32_t first, int32_t count, const void* const
     } else {
       std::memcpy(g.data(), src, (size_t)d * 4);
     }
-    return raw(off, g.data(), (size_t)d * 4);
+    return raw(off, g.data(), (size_t)d * 4, false);
   };
   // Packs src [rows][K] in batches of row tiles through the staging buffers.
   // slot < 0: single-tile strips (tile (r, c) at (r * nkc + c) KiB); slot 0/1:
@@ -533,7 +616,7 @@ int tss_load_weights(tss_ctx* c, int32_t first, int32_t count, const void* const
       hipError_t e = next_stage(&b);
       if (e != hipSuccess) return e;
       pack_tiles(b, (const uint8_t*)src, (r1 - r0) * 16, K, es, kTileBytes,
-                 [&](int n) { return row_map(r0 * 16 + n); });
+                 [&](int n) { return row_map(r0 * 16 + n); }, to_f16, &in_range);
       if (slot < 0)
         e = hipMemcpyAsync(c->w + off + (size_t)r0 * rt_bytes, b, (size_t)(r1 - r0) * rt_bytes, hipMemcpyHostToDevice,
                            c->stream);
@@ -551,7 +634,7 @@ int tss_load_weights(tss_ctx* c, int32_t first, int32_t count, const void* const
     const void* src = host_tensors[i];
     hipError_t e = hipSuccess;
     if (t == 0) {
-      e = raw(c->wl.embed, src, (size_t)v * d * es);
+      e = raw(c->wl.embed, src, (size_t)v * d * es, true);
     } else if (t == 1 + 9 * L) {
       e = gain(c->wl.final_norm, src);
     } else if (t == 2 + 9 * L) {
@@ -574,6 +657,8 @@ int tss_load_weights(tss_ctx* c, int32_t first, int32_t count, const void* const
     if (e != hipSuccess) return hip_fail(c, e, "weight upload");
   }
   HIPCHK(hipStreamSynchronize(c->stream), "weight upload");
+  if (!in_range.load())
+    return fail(c, TSS_EINVAL, "a weight's magnitude exceeds 65504, the largest value of the fp16 operands");
   return TSS_OK;
 }
 

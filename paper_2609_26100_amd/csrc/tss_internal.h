@@ -26,13 +26,14 @@
 //                   [16][hd] (token-major) and a V block [4][hd][4] (token
 //                   t at [t / 4][dim][t % 4]), each 16 * hd elements of KV.
 //
-// Precision modes (T = weight type):
-//   bf16  weights bf16.  GEMM input activations are fp32 values stored as two
-//         bf16 planes, hi = bf16(v) and lo = bf16(v - hi) (planes Mp*K
-//         elements apart); a pair of bf16 MFMAs against the same weight tile
-//         reproduces v * w to about 16 significant bits.  KV cache, q and the
-//         attention probabilities are fp16.  Accumulation, residual stream,
-//         norms, softmax and logits are fp32.
+// Precision modes (T = the packed weights' type):
+//   bf16  the caller's bf16 weights are stored as fp16 (T = _Float16; every
+//         bf16 value of magnitude 2^-17 .. 65504 converts exactly, smaller
+//         ones to the nearest fp16 subnormal, larger ones are refused), and
+//         GEMM input activations are one fp16 plane, so the projections are
+//         fp16 MFMAs (the paper's precision).  KV cache, q and the attention
+//         probabilities are fp16.  Accumulation, residual stream, norms,
+//         softmax and logits are fp32.
 //   f32   everything fp32 (one activation plane, fp32 KV).
 #pragma once
 
@@ -75,9 +76,9 @@ constexpr int kMaxKSplit = 4;
 constexpr int kAttnBatchSlots = 2048;
 
 template <typename T> struct Mode;
-template <> struct Mode<__bf16> {
+template <> struct Mode<_Float16> {
   using KV = _Float16;
-  static constexpr int planes = 2;
+  static constexpr int planes = 1;
 };
 template <> struct Mode<float> {
   using KV = float;
@@ -104,13 +105,14 @@ __device__ __forceinline__ void store_act(void* base, size_t plane, size_t idx, 
     ((T*)base)[idx] = hi;
     ((T*)base)[plane + idx] = (T)(v - (float)hi);
   } else {
-    ((T*)base)[idx] = v;
+    ((T*)base)[idx] = (T)v;
   }
 }
 
 // Stores activations k .. k+3 of one row (k a multiple of 4), which act_index
-// places next to each other in each plane: one 8-byte (bf16 planes) or 16-byte
-// (f32) store per plane instead of one per element.  idx = act_index(row, k).
+// places next to each other in each plane: one 8-byte (16-bit planes) or
+// 16-byte (f32) store per plane instead of one per element.
+// idx = act_index(row, k).
 template <typename T>
 __device__ __forceinline__ void store_act4(void* base, size_t plane, size_t idx, float4 v) {
   if constexpr (Mode<T>::planes == 2) {
@@ -119,8 +121,11 @@ __device__ __forceinline__ void store_act4(void* base, size_t plane, size_t idx,
     typedef T t4 __attribute__((ext_vector_type(4)));
     *(t4*)((T*)base + idx) = t4{h0, h1, h2, h3};
     *(t4*)((T*)base + plane + idx) = t4{l0, l1, l2, l3};
-  } else {
+  } else if constexpr (sizeof(T) == 4) {
     *(float4*)((T*)base + idx) = v;
+  } else {
+    typedef T t4 __attribute__((ext_vector_type(4)));
+    *(t4*)((T*)base + idx) = t4{(T)v.x, (T)v.y, (T)v.z, (T)v.w};
   }
 }
 

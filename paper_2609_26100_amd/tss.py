@@ -29,7 +29,7 @@ EXPORTS = (
     "tss_verify_batch", "tss_verify_sweep", "tss_sweep_prefix_bytes", "tss_get_greedy", "tss_get_path", "tss_seq_length", "tss_seq_truncate", "tss_validate_tree", "tss_validate_mask",
     "tss_tree_meta", "tss_set_launch_mode", "tss_profile_kernel", "tss_profile_read", "tss_last_error", "tss_status_string",
     "tss_destroy", "tss_get_logits_device", "tss_get_attn_split", "tss_check_kv", "tss_verify_static",
-    "tss_static_workspace_bytes",
+    "tss_static_workspace_bytes", "tss_bf16_to_f16",
 )
 
 TSS_STATIC_SCRATCH_BYTES = 64 << 20
@@ -84,6 +84,7 @@ def lib():
             "tss_verify_static": (ctypes.c_int, [P, I32, P, P, I32, P, U32, ctypes.POINTER(I32),
                                                  ctypes.POINTER(I32)]),
             "tss_static_workspace_bytes": (SZ, [CFG]),
+            "tss_bf16_to_f16": (ctypes.c_int64, [P, P, ctypes.c_int64]),
             "tss_get_path": (ctypes.c_int, [P, I32, P, ctypes.POINTER(I32)]),
             "tss_seq_length": (ctypes.c_int, [P, I32, ctypes.POINTER(I32)]),
             "tss_seq_truncate": (ctypes.c_int, [P, I32, I32]),
@@ -197,6 +198,16 @@ def tss_verify_static(ctx, seq, draft_tokens, tree_parent=None, skip_mask=None, 
 
 def tss_static_workspace_bytes(cfg) -> int:
     return lib().tss_static_workspace_bytes(ctypes.byref(cfg))
+
+
+def tss_bf16_to_f16(bits):
+    """bf16 bit patterns (uint16) -> (fp16 bit patterns, count beyond fp16's range)."""
+    src = np.ascontiguousarray(bits, dtype=np.uint16)
+    dst = np.empty_like(src)
+    over = lib().tss_bf16_to_f16(src.ctypes.data, dst.ctypes.data, src.size)
+    if over < 0:
+        raise TSSError(TSS_EINVAL, "tss_bf16_to_f16 refused its arguments")
+    return dst, int(over)
 
 
 def tss_verify_batch(ctx, seq_ids, draft_tokens, node_offsets, tree_parents=None, skip_masks=None, flags=0):

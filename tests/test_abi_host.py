@@ -19,7 +19,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _declared():
     src = open(os.path.join(ROOT, "include", "tss.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(tss_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(tss_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_library_exports_every_declared_symbol():
@@ -166,3 +166,28 @@ def test_static_scratch_sizes():
     bad = abi.make_cfg(synth.TINY)
     bad.head_dim = 96
     assert abi.tss_static_workspace_bytes(bad) == 0
+
+
+def test_bf16_to_f16_every_pattern():
+    """The weight conversion of the bf16 mode, on all 65536 bf16 patterns:
+    the fp16 value numpy's round-to-nearest-even float32 -> float16 cast gives
+    (bf16 -> float32 is exact), NaN for NaN, and the count of finite values
+    beyond fp16's range equal to the patterns of magnitude >= 65536."""
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    got, over = abi.tss_bf16_to_f16(bits)
+    f32 = (bits.astype(np.uint32) << 16).view(np.float32)
+    with np.errstate(over="ignore"):
+        want = f32.astype(np.float16)
+    nan = np.isnan(f32)
+    g = got.view(np.float16)
+    assert np.isnan(g[nan]).all()
+    np.testing.assert_array_equal(got[~nan], want.view(np.uint16)[~nan])
+    assert over == int((np.isfinite(f32) & (np.abs(f32) >= 65536)).sum()) == 2 * (0x7f80 - 0x4780)
+    # exact where fp16 has the value: every bf16 of magnitude 2^-14 .. 65280
+    a = np.abs(f32)
+    exact = (a >= 2.0 ** -14) & (a <= 65280)
+    np.testing.assert_array_equal(g[exact].astype(np.float32), f32[exact])
+    # the subnormal range rounds to the nearest multiple of 2^-24
+    sub = (a > 0) & (a < 2.0 ** -14)
+    assert (np.abs(g[sub].astype(np.float64) - f32[sub]) <= 2.0 ** -25).all()
+    assert abi.tss_bf16_to_f16(np.zeros(0, np.uint16))[1] == 0
