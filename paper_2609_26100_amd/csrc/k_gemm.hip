@@ -103,6 +103,22 @@ constexpr size_t gemm_lds(int waves) {
   return (size_t)(waves * MT * 16 * red_cols<MT, NT>() + 2 * MT * 16 * NT * 16 + MT * 16) * 4;
 }
 
+// Epilogue operands of the one-row-tile residual epilogue (one output item
+// per thread): h and, when every row belongs to segment 0, the next norm's
+// gain, requested after the wave's last weight chunk, so no weight load waits
+// behind them, and in flight while the last MFMAs and the cross-wave
+// reduction run.  Their addresses need no other load, and every thread loads
+// (its index clamped to a valid item), so the load-count waits stay exact.
+template <int EPI, int MT, int COLS>
+__device__ __forceinline__ void prefetch_epilogue(const GemmArgs& a, int M, int n0, float4& pre_h, float4& pre_g) {
+  if constexpr (EPI == EPI_RESID && MT == 1) {
+    const int e4 = min((int)threadIdx.x, M * COLS / 4 - 1);
+    const int row = e4 / (COLS / 4), col = (e4 % (COLS / 4)) * 4;
+    pre_h = *(const float4*)(a.h + (size_t)row * a.N + n0 + col);
+    pre_g = *(const float4*)(a.g_next[0] + n0 + col);
+  }
+}
+
 template <typename T, int MT, int NT, int EPI>
 __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
@@ -227,6 +243,10 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
 #pragma unroll
         for (int p = 0; p < S; ++p) acc[mt][nt] = mfma_chunk<T>(xs[mt][p], w[nt], acc[mt][nt]);
   };
+  // epilogue operands prefetched after the weight stream (prefetch_epilogue)
+  constexpr bool PRE_RESID = EPI == EPI_RESID && MT == 1;
+  float4 pre_h = make_float4(0.f, 0.f, 0.f, 0.f), pre_g = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int n0 = strip * COLS;
   if (n_my > 0) {
 #pragma unroll
     for (int j = 0; j < D; ++j) issue(wv[j], xv[j], min(j, n_my - 1));
@@ -246,9 +266,12 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
         if (i0 + j + D < n_my) issue(wv[j], xv[j], i0 + j + D);
       }
     }
+    prefetch_epilogue<EPI, MT, COLS>(a, M, n0, pre_h, pre_g);
 #pragma unroll
     for (int j = 0; j < D; ++j)
       if (i0 + D + j < n_my) compute(wv[j], xv[j]);
+  } else {
+    prefetch_epilogue<EPI, MT, COLS>(a, M, n0, pre_h, pre_g);
   }
 
   // LDS: red[waves][ROWS][RC] | yfin[ROWS][COLS] | aux[ROWS][COLS] | rscale[ROWS].
@@ -364,7 +387,6 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) yfin[e] *= rscale[e / COLS];
   __syncthreads();
 
-  const int n0 = strip * COLS;
   if constexpr (EPI == EPI_QKV) {
     const int HD = a.head_dim, d = a.d;
     const int d16 = d >> 4, hd16 = HD >> 4;
@@ -407,11 +429,20 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       const int row = e4 / (COLS / 4), col = (e4 % (COLS / 4)) * 4;
       if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
       const size_t idx = (size_t)row * N + n0 + col;
-      const float4 h0 = *(const float4*)(a.h + idx);
+      // one pass (always with one row tile): the operands prefetched for e4
+      const bool pre = PRE_RESID && M * COLS / 4 <= (int)blockDim.x;
+      float4 h0, gn;
+      if (pre)
+        h0 = pre_h;
+      else
+        h0 = *(const float4*)(a.h + idx);
       const float* y = yfin + row * COLS + col;
       const float4 hn = make_float4(h0.x + y[0], h0.y + y[1], h0.z + y[2], h0.w + y[3]);
       *(float4*)(a.h + idx) = hn;
-      const float4 gn = *(const float4*)(a.g_next[s_seq[row]] + n0 + col);
+      if (pre && a.n_seqs == 1)
+        gn = pre_g;
+      else
+        gn = *(const float4*)(a.g_next[s_seq[row]] + n0 + col);
       store_act4<T>(a.xn, a.xn_plane, act_index<T>(row, n0 + col, N),
                     make_float4(hn.x * gn.x, hn.y * gn.y, hn.z * gn.z, hn.w * gn.w));
       *(float4*)(aux + row * COLS + col) = make_float4(hn.x * hn.x, hn.y * hn.y, hn.z * hn.z, hn.w * hn.w);
