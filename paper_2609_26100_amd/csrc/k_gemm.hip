@@ -243,10 +243,10 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
 #pragma unroll
         for (int p = 0; p < S; ++p) acc[mt][nt] = mfma_chunk<T>(xs[mt][p], w[nt], acc[mt][nt]);
   };
-  // epilogue operands prefetched after the weight stream (prefetch_epilogue)
+  // epilogue operands prefetched after the weight stream (prefetch_epilogue;
+  // a wave without chunks loads them in the epilogue)
   constexpr bool PRE_RESID = EPI == EPI_RESID && MT == 1;
   float4 pre_h = make_float4(0.f, 0.f, 0.f, 0.f), pre_g = make_float4(0.f, 0.f, 0.f, 0.f);
-  const int n0 = strip * COLS;
   if (n_my > 0) {
 #pragma unroll
     for (int j = 0; j < D; ++j) issue(wv[j], xv[j], min(j, n_my - 1));
@@ -266,12 +266,10 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
         if (i0 + j + D < n_my) issue(wv[j], xv[j], i0 + j + D);
       }
     }
-    prefetch_epilogue<EPI, MT, COLS>(a, M, n0, pre_h, pre_g);
+    if constexpr (PRE_RESID) prefetch_epilogue<EPI, MT, COLS>(a, M, strip * COLS, pre_h, pre_g);
 #pragma unroll
     for (int j = 0; j < D; ++j)
       if (i0 + D + j < n_my) compute(wv[j], xv[j]);
-  } else {
-    prefetch_epilogue<EPI, MT, COLS>(a, M, n0, pre_h, pre_g);
   }
 
   // LDS: red[waves][ROWS][RC] | yfin[ROWS][COLS] | aux[ROWS][COLS] | rscale[ROWS].
@@ -387,6 +385,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) yfin[e] *= rscale[e / COLS];
   __syncthreads();
 
+  const int n0 = strip * COLS;
   if constexpr (EPI == EPI_QKV) {
     const int HD = a.head_dim, d = a.d;
     const int d16 = d >> 4, hd16 = HD >> 4;
@@ -430,7 +429,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
       const size_t idx = (size_t)row * N + n0 + col;
       // one pass (always with one row tile): the operands prefetched for e4
-      const bool pre = PRE_RESID && M * COLS / 4 <= (int)blockDim.x;
+      const bool pre = PRE_RESID && M * COLS / 4 <= (int)blockDim.x && n_my > 0;
       float4 h0, gn;
       if (pre)
         h0 = pre_h;

@@ -96,68 +96,89 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return (nv && !nb) || v > bv || ((v == bv || (nv && nb)) && i < bi);
 }
 
-// One workgroup of 16 waves.  Greedy token per row from the lm_head's
-// per-strip partials (each row gets 16 / M waves, loads issued eight at a
-// time), then one accept scan per sequence over its tree: a node is accepted
-// when its parent is and its token equals the parent's greedy token; the
-// deepest accepted node (lowest id among equal depths) gives accept_len and
-// the bonus token.
-__global__ __launch_bounds__(1024) void k_accept(AcceptArgs a) {
+// Greedy token per row, one workgroup of 256 threads per row: each thread
+// reduces its share of the lm_head's per-strip (max, argmax) partials (all of
+// its loads issued together), then the wave and the workgroup combine theirs
+// in a fixed order (the order of `better` is total, so the result does not
+// depend on it anyway).  The rows' greedy tokens are published with
+// agent-scope stores; the last workgroup to arrive (a counter bumped after
+// the store has landed) runs one accept scan per sequence over its tree: a
+// node is accepted when its parent is and its token equals the parent's
+// greedy token; the deepest accepted node (lowest id among equal depths)
+// gives accept_len and the bonus token.
+constexpr int kAcceptThreads = 256;
+constexpr int kAcceptLoads = 8;  // partials per thread per round (2048 per round: V = 32000 in one)
+__global__ __launch_bounds__(kAcceptThreads) void k_accept(AcceptArgs a) {
+  __shared__ float bvs[kAcceptThreads / 64];
+  __shared__ int32_t bis[kAcceptThreads / 64];
+  __shared__ int last;
   __shared__ int32_t g[kMaxRows];
-  __shared__ float bvs[16];
-  __shared__ int32_t bis[16];
   __shared__ int32_t s_tok[kMaxRows];
   __shared__ int8_t s_par[kMaxRows];
   __shared__ uint8_t s_dep[kMaxRows];
+  const int m = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int M = a.M;
-  if (threadIdx.x < M) {
-    s_tok[threadIdx.x] = a.sp->tok[threadIdx.x];
-    s_par[threadIdx.x] = a.sp->parent[threadIdx.x];
-    s_dep[threadIdx.x] = a.sp->depth[threadIdx.x];
-  }
-  const int wpr = M >= 16 ? 1 : (M >= 8 ? 2 : (M >= 4 ? 4 : (M >= 2 ? 8 : 16)));  // waves per row
-  const int groups = 16 / wpr;
-  const int grp_id = wave / wpr, sub = wave % wpr;
-  for (int m0 = 0; m0 < M; m0 += groups) {
-    const int m = m0 + grp_id;
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-    if (m < M) {
-      const int stride = 64 * wpr;
-      for (int p = sub * 64 + lane; p < a.nparts; p += 8 * stride) {
-        float v[8];
-        int ix[8];
+  // the row's partials through buffer resources: loads past the row return
+  // zeros (replaced below), so none needs a branch
+  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.am_val + (size_t)m * a.am_stride), (short)0, a.nparts * 4, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ires = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.am_idx + (size_t)m * a.am_stride), (short)0, a.nparts * 4, 0x00020000);
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int p0 = threadIdx.x; p0 < a.nparts; p0 += kAcceptLoads * kAcceptThreads) {
+    float v[kAcceptLoads];
+    int ix[kAcceptLoads];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int q = p + u * stride;
-          v[u] = q < a.nparts ? a.am_val[(size_t)m * a.am_stride + q] : -INFINITY;
-          ix[u] = q < a.nparts ? a.am_idx[(size_t)m * a.am_stride + q] : 0x7fffffff;
-        }
+    for (int u = 0; u < kAcceptLoads; ++u) {
+      const int q = p0 + u * kAcceptThreads;
+      v[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(vres, q * 4, 0, 0));
+      ix[u] = (int)__builtin_amdgcn_raw_buffer_load_b32(ires, q * 4, 0, 0);
+    }
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (better(v[u], ix[u], bv, bi)) { bv = v[u]; bi = ix[u]; }
+    for (int u = 0; u < kAcceptLoads; ++u) {
+      const bool in = p0 + u * kAcceptThreads < a.nparts;
+      if (in && better(v[u], ix[u], bv, bi)) {
+        bv = v[u];
+        bi = ix[u];
       }
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      const float ov = __shfl_xor(bv, off);
-      const int oi = __shfl_xor(bi, off);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
-    if (lane == 0) {
-      bvs[wave] = bv;
-      bis[wave] = bi;
-    }
-    __syncthreads();
-    if (sub == 0 && lane == 0 && m < M) {
-      for (int w = 1; w < wpr; ++w)
-        if (better(bvs[wave + w], bis[wave + w], bv, bi)) { bv = bvs[wave + w]; bi = bis[wave + w]; }
-      g[m] = bi;
-      a.greedy[m] = bi;
-    }
-    __syncthreads();
   }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ov = __shfl_xor(bv, off);
+    const int oi = __shfl_xor(bi, off);
+    if (better(ov, oi, bv, bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  if (lane == 0) {
+    bvs[wave] = bv;
+    bis[wave] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kAcceptThreads / 64; ++w)
+      if (better(bvs[w], bis[w], bv, bi)) {
+        bv = bvs[w];
+        bi = bis[w];
+      }
+    __hip_atomic_store(a.greedy + m, bi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    last = __hip_atomic_fetch_add(a.count, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (int)gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+
+  const int M = a.M;
+  for (int i = threadIdx.x; i < M; i += kAcceptThreads) {
+    g[i] = __hip_atomic_load(a.greedy + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_tok[i] = a.sp->tok[i];
+    s_par[i] = a.sp->parent[i];
+    s_dep[i] = a.sp->depth[i];
+  }
+  __syncthreads();
   const int sq = threadIdx.x;
   if (sq < a.sp->n_seqs) {
     const int r0 = a.sp->seq_row0[sq], n = a.sp->seq_row0[sq + 1] - r0;
@@ -184,6 +205,7 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a) {
       }
     }
   }
+  if (threadIdx.x == 0) *a.count = 0;
 }
 
 // Moves the K/V of an accepted tree path (local nodes path[1..a]) to the
@@ -248,7 +270,8 @@ hipError_t launch_embed(bool bf16, const EmbedArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
-  TSS_LAUNCH(k_accept, dim3(1), dim3(1024), 0, s, a);
+  if (a.M < 1 || a.M > kMaxRows || !a.count) return hipErrorInvalidValue;
+  TSS_LAUNCH(k_accept, dim3(a.M), dim3(kAcceptThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -44,7 +44,7 @@ struct WeightLayout {
 };
 
 struct WsLayout {
-  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, counters, attn_split, kpart, kcount, logits,
+  size_t sp, result, h, xa, xm, ss_a, ss_m, q, o, act, part_o, part_ml, counters, attn_split, kpart, kcount, acount, logits,
       am_val, am_idx, greedy, total;
   int n_counters;
 };
@@ -204,11 +204,12 @@ WsLayout ws_layout(const tss_model_cfg* c) {
   const size_t slots = attn_slots(c);
   w.part_o = take(slots * kAttnMaxTiles * 16 * c->head_dim * 4);
   w.part_ml = take(slots * kAttnMaxTiles * 16 * 2 * 4);
-  // arrival counters of the attention merges and of the K-split strips, one
-  // region that every step clears first (embedding kernel)
-  w.counters = take((size_t)c->n_heads * kAttnMaxItems * 4 + (d / 16) * 4);
+  // arrival counters of the attention merges, of the K-split strips and of
+  // the argmax rows, one region that every step clears first (embedding kernel)
+  w.counters = take((size_t)c->n_heads * kAttnMaxItems * 4 + (d / 16) * 4 + 4);
   w.kcount = w.counters + (size_t)c->n_heads * kAttnMaxItems * 4;
-  w.n_counters = c->n_heads * kAttnMaxItems + (int)(d / 16);
+  w.acount = w.kcount + (d / 16) * 4;
+  w.n_counters = c->n_heads * kAttnMaxItems + (int)(d / 16) + 1;
   w.attn_split = take((2 * kAttnMaxItems + 1) * 4);
   w.kpart = take((size_t)kMaxKSplit * d * Mp * 4);  // K-split partial products of the residual projections
   w.logits = take(Mp * v * 4);
@@ -1033,6 +1034,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
       a.am_stride = cf.vocab / 16;
       a.sp = sp_dev;
       a.greedy = (int32_t*)(ws + c->wsl.greedy);
+      a.count = (int*)(ws + c->wsl.acount);
       a.result = (Result*)(ws + c->wsl.result);
       a.result_host = c->res_dev_map;
       ProfScope ps(c, TSS_K_ACCEPT, -1);

@@ -272,7 +272,8 @@ struct AcceptArgs {
   const int32_t* am_idx;
   int nparts, M, am_stride;
   const StepParams* sp;
-  int32_t* greedy;         // [Mp]
+  int32_t* greedy;         // [Mp] (agent-scope stores: the last row's workgroup reads them all)
+  int* count;              // rows finished, zero between launches
   Result* result;          // [n_seqs] device copy, one per segment (read by the compaction kernel)
   Result* result_host;     // [n_seqs] host-mapped pinned copy (read by the host after the step)
 };
