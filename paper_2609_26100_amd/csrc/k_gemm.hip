@@ -293,6 +293,12 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     if (lane == 0) rscale[wave] = rsqrtf(s / (float)a.norm_dim + a.eps);
   }
 
+  // When the row scale is known before the sums (loaded early, or no norm),
+  // it is applied as they are written (the same product as applying it
+  // afterwards), which saves a pass over the block and a barrier.  The
+  // residual projections (no norm, possibly K-split) always fold.
+  const bool fold = ss_early || !a.ss_in;
+
   // MFMA result layout: lane holds column r16, rows 4*grp + v.
 #pragma unroll
   for (int c0 = 0; c0 < COLS; c0 += RC) {
@@ -309,7 +315,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       const int row = e / RC, col = e % RC;
       float s = 0.f;
       for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * RC + col];
-      yfin[row * COLS + c0 + col] = s;
+      yfin[row * COLS + c0 + col] = fold && a.ss_in ? s * rscale[row] : s;
     }
   }
 
@@ -351,38 +357,34 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     if (threadIdx.x == 0) a.kcount[strip] = 0;
   }
 
-  if (!ss_early) {
-    if (a.ss_in) {
-      // rows in groups of 4 per wave, every load of a group issued together
-      // (indices clamped, out-of-range parts weighted 0)
-      for (int m0 = wave; m0 < M; m0 += 4 * waves) {
-        float sum[4];
+  if (!fold) {
+    // rows in groups of 4 per wave, every load of a group issued together
+    // (indices clamped, out-of-range parts weighted 0)
+    for (int m0 = wave; m0 < M; m0 += 4 * waves) {
+      float sum[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = min(m0 + r * waves, M - 1);
-          float v[SSV];
+      for (int r = 0; r < 4; ++r) {
+        const int m = min(m0 + r * waves, M - 1);
+        float v[SSV];
 #pragma unroll
-          for (int i = 0; i < SSV; ++i) v[i] = a.ss_in[(size_t)m * a.ss_stride + min(lane + 64 * i, a.ss_nparts - 1)];
-          float t = 0.f;
+        for (int i = 0; i < SSV; ++i) v[i] = a.ss_in[(size_t)m * a.ss_stride + min(lane + 64 * i, a.ss_nparts - 1)];
+        float t = 0.f;
 #pragma unroll
-          for (int i = 0; i < SSV; ++i) t += lane + 64 * i < a.ss_nparts ? v[i] : 0.f;
-          sum[r] = t;
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float t = sum[r];
-#pragma unroll
-          for (int off = 32; off >= 1; off >>= 1) t += __shfl_xor(t, off);
-          const int m = m0 + r * waves;
-          if (lane == 0 && m < M) rscale[m] = rsqrtf(t / (float)a.norm_dim + a.eps);
-        }
+        for (int i = 0; i < SSV; ++i) t += lane + 64 * i < a.ss_nparts ? v[i] : 0.f;
+        sum[r] = t;
       }
-    } else {
-      for (int m = threadIdx.x; m < M; m += blockDim.x) rscale[m] = 1.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float t = sum[r];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) t += __shfl_xor(t, off);
+        const int m = m0 + r * waves;
+        if (lane == 0 && m < M) rscale[m] = rsqrtf(t / (float)a.norm_dim + a.eps);
+      }
     }
+    __syncthreads();
+    for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) yfin[e] *= rscale[e / COLS];
   }
-  __syncthreads();
-  for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) yfin[e] *= rscale[e / COLS];
   __syncthreads();
 
   const int n0 = strip * COLS;
