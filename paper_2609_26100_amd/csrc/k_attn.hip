@@ -120,13 +120,18 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < NV; ++c) vreg[c] = vp[c];
   };
-  // Page p of the item's sequence.  p is uniform: the argument list is read
-  // with a scalar load, and only pages past it read the page table (a
-  // uniform branch, so that read's wait never holds back an argument page).
-  auto load_page = [&](int p, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
+  // Page p of the item's sequence, the wave's it-th page.  p is uniform: the
+  // argument list is read with a scalar load; pages past it take their id
+  // from `ids` (lane it holds the id of the wave's it-th page, read with one
+  // vector load before the walk, so the walk never waits on a page-table
+  // read) or, past the wave's 64th page, from the page table.
+  int ids = 0;
+  auto load_page = [&](int p, int it, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
     int phys;
     if (p < arg_pages)
       phys = a.pages[p];
+    else if (it < 64)
+      phys = __builtin_amdgcn_readlane(ids, it);
     else
       phys = __builtin_amdgcn_readfirstlane(__builtin_nontemporal_load(pt + p));
     load_phys(phys, kreg, vreg);
@@ -162,6 +167,11 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     return;
   }
   pt = a.page_table + a.pt_off[sq];
+  const int stride = W * G;
+  if (n_pages > arg_pages) {  // uniform: some page of the item lies past the argument list
+    const int pp = p + lane * stride;
+    if (pp < n_pages && pp >= arg_pages) ids = __builtin_nontemporal_load(pt + pp);
+  }
 
   // B operand of S = K Q^T for tile t: lane (node 16 t + r16, group grp)
   // holds q[node][head*HD + grp*DL + 0..DL).  Waves 0..T-1 build one tile
@@ -215,12 +225,11 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     for (int n = 0; n < NO; ++n) O[t][n] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  const int stride = W * G;
-  if (!early && p < n_pages) load_page(p, kcur, vcur);
+  if (!early && p < n_pages) load_page(p, 0, kcur, vcur);
   __syncthreads();  // q tiles ready
-  for (; p < n_pages; p += stride) {
+  for (int it = 0; p < n_pages; p += stride, ++it) {
     uint4 knext[NQ], vnext[NV];
-    if (p + stride < n_pages) load_page(p + stride, knext, vnext);
+    if (p + stride < n_pages) load_page(p + stride, it + 1, knext, vnext);
 
 #pragma unroll
     for (int t = 0; t < TMAX; ++t) {
