@@ -28,12 +28,17 @@
 //     (v_mfma_f32_16x16x32_f16 for S, v_mfma_f32_16x16x16_f16 for P V) in the
 //     bf16 mode; fp32 throughout (v_mfma_f32_16x16x4_f32) in the f32 mode.
 // The 8 waves' softmax states meet in LDS (fixed order), tile after tile.
-// With G = 1 the workgroup writes the normalised rows itself.  With G > 1
-// each workgroup writes its partial states with agent-scope stores, waits
-// for them to land, and bumps a per-(head, sequence) counter; the last to
-// arrive reads them with agent-scope loads and merges the G partials in
-// workgroup order and resets the counter.  No second kernel (a kernel
-// boundary costs about 3 us on this GPU) and bit-reproducible results.
+// With G = 1 the workgroup writes the normalised rows itself.  With G > 1,
+// in launches of single-tile items, each workgroup writes its partial states
+// with agent-scope stores, waits for them to land, and bumps a per-(head,
+// sequence) counter; the last to arrive reads them with agent-scope loads and
+// merges the G partials in workgroup order and resets the counter (no second
+// kernel: a kernel boundary costs about as much as this hand-over).  Items of
+// several row tiles have too many partial states for one workgroup to read
+// quickly (256 KiB at four tiles and eight workgroups: 8.4 us), so their
+// launches leave the partial states to k_attn_merge, a second launch in which
+// each workgroup merges 8 rows of one (head, item).  Either way the order of
+// summation is fixed: results are bit-reproducible.
 //
 // An item's G (at most `groups`, at least one page per wave, at most
 // pages / (4 T), and in a batch of sequences one per `pages_per_wg` pages) is
@@ -80,6 +85,15 @@ __device__ __forceinline__ float4 load_agent4(__amdgpu_buffer_rsrc_t r, int off)
 #define TSS_ATTN_PART_DIV 4
 #endif
 constexpr int kAttnWaves = TSS_ATTN_WAVES;
+
+// Workgroups an item's n_pages pages are divided among: at most `groups`, at
+// least a page per wave, few enough that the partial states (T tiles each)
+// stay well below the pages, and in a batch of sequences one per
+// pages_per_wg pages.  The attention and merge launches derive it alike.
+__device__ __forceinline__ int attn_item_groups(const AttnArgs& a, int n_pages, int T) {
+  const int cap = a.pages_per_wg > 0 ? min(a.groups, (n_pages + a.pages_per_wg - 1) / a.pages_per_wg) : a.groups;
+  return max(1, min(cap, min((n_pages + kAttnWaves - 1) / kAttnWaves, n_pages / (TSS_ATTN_PART_DIV * T))));
+}
 
 // LDS: q tiles [TMAX][64][NQ] uint4 | m, l [W][16] | O [W][64][OS]
 template <typename TK, int HD, int TMAX>
@@ -153,10 +167,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   const int Ms = a.item_rows[y];                     // rows of the item
   const int T = (Ms + 15) >> 4;                      // its row tiles (<= TMAX)
   const int n_pages = (n_kv + a.item_slots[y] + kPage - 1) / kPage;
-  // workgroups of this item: at most groups, at least a page per wave, and
-  // few enough that partial states (T tiles each) stay well below the pages
-  const int cap = a.pages_per_wg > 0 ? min(a.groups, (n_pages + a.pages_per_wg - 1) / a.pages_per_wg) : a.groups;
-  const int G = max(1, min(cap, min((n_pages + W - 1) / W, n_pages / (TSS_ATTN_PART_DIV * T))));
+  const int G = attn_item_groups(a, n_pages, T);
   if (head == 0 && g == 0 && threadIdx.x == 0) {  // the split this launch took (inspection)
     a.split_out[y] = G;
     a.split_out[kAttnMaxItems + y] = Ms;
@@ -334,6 +345,9 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     return make_float2(mx, den);
   };
   const size_t slot = ((size_t)head * gridDim.y + y) * a.groups + g;  // this workgroup's partial slot
+  // items of several row tiles leave their partial states to k_attn_merge
+  // (plain stores: the kernel boundary publishes them)
+  const bool defer = a.defer_merge != 0;
   // the partial outputs of the launch: [heads * items * groups][TMAX][16][HD] floats
   const __amdgpu_buffer_rsrc_t pres = __builtin_amdgcn_make_buffer_rsrc(
       a.part_o, (short)0, (int)((size_t)a.n_heads * gridDim.y * a.groups * TMAX * 16 * HD * sizeof(float)), 0x00020000);
@@ -376,6 +390,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
         const float den = md.y;
         store_act4<TW>(a.o, a.o_plane, act_index<TW>(row0 + ln, head * HD + dim, a.d),
                        make_float4(num.x / den, num.y / den, num.z / den, num.w / den));
+      } else if (defer) {
+        *(float4*)(a.part_o + (slot * TMAX + t) * 16 * HD + row * HD + dim) = num;
       } else {
         store_agent4(pres, (int)(((slot * TMAX + t) * 16 * HD + row * HD + dim) * sizeof(float)), num);
       }
@@ -383,12 +399,16 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
     if (G > 1 && threadIdx.x < 16) {
       float f[W];
       const float2 md = row_weights(threadIdx.x, f);
-      store_agent(pm + threadIdx.x * 2 + 0, md.x);
-      store_agent(pm + threadIdx.x * 2 + 1, md.y);
+      if (defer) {
+        *(float2*)(pm + threadIdx.x * 2) = md;
+      } else {
+        store_agent(pm + threadIdx.x * 2 + 0, md.x);
+        store_agent(pm + threadIdx.x * 2 + 1, md.y);
+      }
     }
     __syncthreads();  // the next tile reuses the merge buffers
   }
-  if (G == 1) return;
+  if (G == 1 || defer) return;
 
   // Publish this workgroup's partials, then let the last arrival merge.  Each
   // thread waits until its agent-scope stores are acknowledged (then they are
@@ -493,6 +513,55 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   if (threadIdx.x == 0) a.counters[ctr] = 0;
 }
 
+// The deferred merge: workgroup (head, item, z) combines rows 8 z .. 8 z + 7
+// of the item from its G partial states (plain loads: the attention launch
+// has ended), one thread per four adjacent dimensions of a row, summed in
+// workgroup order; items the attention launch finished itself (G = 1) are
+// skipped.
+constexpr int kMergeRows = 8;
+template <typename TW, int HD, int TMAX>
+__global__ __launch_bounds__(kMergeRows * HD / 4) void k_attn_merge(AttnArgs a) {
+  const int head = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  const int row0 = a.item_row0[y], Ms = a.item_rows[y];
+  const int lr = z * kMergeRows + (int)threadIdx.x / (HD / 4);  // row of the item
+  if (lr >= Ms) return;
+  const int T = (Ms + 15) >> 4;
+  const int G = attn_item_groups(a, (a.sp->seq_nkv[a.item_seg[y]] + a.item_slots[y] + kPage - 1) / kPage, T);
+  if (G == 1) return;
+  const int dim = ((int)threadIdx.x % (HD / 4)) * 4;
+  const int t = lr >> 4, row = lr & 15;
+  const size_t slot0 = ((size_t)head * gridDim.y + y) * a.groups;
+  float2 ml[kAttnMaxGroups];
+  float4 o[kAttnMaxGroups];
+#pragma unroll
+  for (int k = 0; k < kAttnMaxGroups; ++k) {
+    if (k < G) {
+      const size_t sl = (slot0 + k) * TMAX + t;
+      ml[k] = *(const float2*)(a.part_ml + sl * 32 + row * 2);
+      o[k] = *(const float4*)(a.part_o + sl * 16 * HD + row * HD + dim);
+    }
+  }
+  float mx = -1e30f;
+#pragma unroll
+  for (int k = 0; k < kAttnMaxGroups; ++k)
+    if (k < G) mx = fmaxf(mx, ml[k].x);
+  float den = 0.f;
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int k = 0; k < kAttnMaxGroups; ++k) {
+    if (k < G) {
+      const float f = exp2f(ml[k].x - mx);
+      den += f * ml[k].y;
+      num.x += f * o[k].x;
+      num.y += f * o[k].y;
+      num.z += f * o[k].z;
+      num.w += f * o[k].w;
+    }
+  }
+  store_act4<TW>(a.o, a.o_plane, act_index<TW>(row0 + lr, head * HD + dim, a.d),
+                 make_float4(num.x / den, num.y / den, num.z / den, num.w / den));
+}
+
 template <typename TK, typename TW, int HD, int TMAX>
 static hipError_t attn_attr() {
   return hipFuncSetAttribute((const void*)k_attn<TK, TW, HD, TMAX>, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -521,7 +590,13 @@ template <typename TK, typename TW, int HD, int TMAX>
 static hipError_t attn_t(int n_seq, const AttnArgs& a, hipStream_t s) {
   const size_t lds = attn_lds<TK, HD, TMAX>();
   TSS_LAUNCH((k_attn<TK, TW, HD, TMAX>), dim3(a.n_heads, n_seq, a.groups), dim3(kAttnWaves * 64), lds, s, a);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && a.defer_merge) {
+    TSS_LAUNCH((k_attn_merge<TW, HD, TMAX>), dim3(a.n_heads, n_seq, TMAX * 16 / kMergeRows),
+               dim3(kMergeRows * HD / 4), 0, s, a);
+    e = hipGetLastError();
+  }
+  return e;
 }
 
 template <typename TK, typename TW, int HD>

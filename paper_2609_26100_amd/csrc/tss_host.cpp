@@ -942,6 +942,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
         a.groups = attn_groups(H, n_act);
         a.pages_per_wg = 0;
       }
+      a.defer_merge = max_tiles >= 2;
       a.layer = l;
       a.n_pages_pool = c->kvl.n_pages;
       a.n_heads = H;

@@ -235,6 +235,7 @@ struct AttnArgs {
   int32_t* split_out;
   int groups;              // most workgroups per (head, item)
   int pages_per_wg;        // > 0: an item takes ceil(pages / pages_per_wg) workgroups (at most groups)
+  int defer_merge;         // partial states merged by a second launch (launches with items of 2+ row tiles)
   int layer, n_pages_pool, n_heads, d;
   float scale_log2;        // log2(e) / sqrt(hd)
   // per item, 32-bit so that the kernel reads them with scalar loads
