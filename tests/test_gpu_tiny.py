@@ -407,3 +407,36 @@ def test_logits_device_copy_and_split_report(pair):
     assert v.attn_split() == []
     res = verify(m, o, tok, mask=np.ones(L, np.uint8))
     assert float(np.max(np.abs(v.logits(6) - res.logits))) <= 1e-4
+
+
+def test_context_past_the_argument_pages():
+    """A single sequence whose context outgrows the page ids passed in the kernel arguments (4500 tokens:
+    282 pages, 256 of them in the arguments): the pages past the list come from the page table, read once
+    per wave before its walk.  Chain and tree steps against the oracle, and a committing step followed by
+    another verify."""
+    from tests.gpu_common import prefill_chunked
+    n = 4500
+    v = gpu_verifier(SHAPE, random_gains=True, n_seqs=1, max_tokens=n + 80, max_nodes=64)
+    m = oracle_model(SHAPE, random_gains=True)
+    try:
+        mask = synth.mask_from_layers(L, [1])
+        toks = synth.context_tokens(SHAPE.vocab, n + 20, stream=61)
+        v.set_mask(0, mask)
+        v.prefill(0, toks[:n])
+        o = OracleSequence(m, mask)
+        prefill_chunked(m, o, toks[:n])
+        tok = np.concatenate([[toks[n]], synth.context_tokens(SHAPE.vocab, 5, stream=62)])
+        _, _, err, _ = compare_step(SHAPE, v, 0, m, o, tok)
+        log(f"{n}-token context, chain: logits err {err:.2e}")
+        parent = synth.random_tree(16, stream=63)
+        tok = np.concatenate([[toks[n]], synth.context_tokens(SHAPE.vocab, 15, stream=64)])
+        _, _, err, _ = compare_step(SHAPE, v, 0, m, o, tok, parent)
+        log(f"{n}-token context, 16-node tree: logits err {err:.2e}")
+        tok = np.concatenate([[toks[n]], synth.context_tokens(SHAPE.vocab, 5, stream=65)])
+        res, (al, nt), err, _ = compare_step(SHAPE, v, 0, m, o, tok, commit=True)
+        assert v.length(0) == o.n_kv == n + al + 1
+        tok = np.concatenate([[nt], synth.context_tokens(SHAPE.vocab, 5, stream=66)])
+        _, _, err2, _ = compare_step(SHAPE, v, 0, m, o, tok)
+        log(f"after a commit (n_kv {o.n_kv}): logits err {err:.2e} / {err2:.2e}")
+    finally:
+        v.close()
