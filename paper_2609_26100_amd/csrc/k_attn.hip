@@ -57,6 +57,25 @@ __device__ __forceinline__ unsigned pack_f16x2(float lo, float hi) {
   return (unsigned)__builtin_bit_cast(unsigned short, a) | ((unsigned)__builtin_bit_cast(unsigned short, b) << 16);
 }
 
+// Reductions over the four lanes l, l^16, l^32, l^48 of a node column with
+// gfx950's row-swap permutes (VALU, no trip through the LDS pipeline): given
+// one value twice, v_permlane16_swap leaves a lane its own value and that of
+// the lane 16 away, v_permlane32_swap its own and that of the lane 32 away.
+// Max and sum are commutative, so every lane gets the same bits as with
+// pairwise exchanges.
+__device__ __forceinline__ float max_col4(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  const auto h = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(h[0]), __uint_as_float(h[1]));
+}
+__device__ __forceinline__ float sum_col4(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  const auto h = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(h[0]) + __uint_as_float(h[1]);
+}
+
 // Partial states travel between workgroups (possibly on different XCDs, whose
 // L2 caches are not coherent with each other) through agent-scope accesses:
 // the stores write through to the level every XCD sees and the loads read
@@ -237,6 +256,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   }
 
   if (!early && p < n_pages) load_page(p, 0, kcur, vcur);
+  float* sm_alpha = smem + TMAX * 64 * NQ * 4 + wave * 16;  // the wave's slots of the merge's m array
   __syncthreads();  // q tiles ready
   for (int it = 0; p < n_pages; p += stride, ++it) {
     uint4 knext[NQ], vnext[NV];
@@ -262,44 +282,58 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       }
 
       // S[v] = score of token 4*grp+v of this page against local node 16 t + r16.
+      // Only pages that reach past the context hold draft slots, whose
+      // visibility depends on the node (p is uniform, so is the branch).
       float s[4];
-      float mloc = -INFINITY;
+      float mloc;
+      if ((p + 1) * kPage <= n_kv) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int slot = p * kPage + grp * 4 + v;
-        bool vis;
-        if (slot < n_kv) {
-          vis = true;
-        } else {
-          const unsigned j = (unsigned)(slot - n_kv - base[t]);
-          vis = j < 64u && ((anc[t] >> j) & 1ull);
+        for (int v = 0; v < 4; ++v) s[v] = S[v] * a.scale_log2;
+        mloc = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+      } else {
+        mloc = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int slot = p * kPage + grp * 4 + v;
+          bool vis;
+          if (slot < n_kv) {
+            vis = true;
+          } else {
+            const unsigned j = (unsigned)(slot - n_kv - base[t]);
+            vis = j < 64u && ((anc[t] >> j) & 1ull);
+          }
+          s[v] = vis ? S[v] * a.scale_log2 : -INFINITY;
+          mloc = fmaxf(mloc, s[v]);
         }
-        s[v] = vis ? S[v] * a.scale_log2 : -INFINITY;
-        mloc = fmaxf(mloc, s[v]);
       }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-      const float m_new = fmaxf(m_run[t], mloc);
-      const float alpha = exp2f(m_run[t] - m_new);
+      // exponentials with the bare v_exp_f32 (results below 2^-126 flush to
+      // zero, which no probability or weight here needs)
+      const float m_new = fmaxf(m_run[t], max_col4(mloc));
+      const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_new);
       float pv[4];
       float lsum = 0.f;
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        pv[v] = exp2f(s[v] - m_new);
+        pv[v] = __builtin_amdgcn_exp2f(s[v] - m_new);
         lsum += pv[v];
       }
-      lsum += __shfl_xor(lsum, 16);
-      lsum += __shfl_xor(lsum, 32);
-      l_run[t] = l_run[t] * alpha + lsum;
+      l_run[t] = l_run[t] * alpha + sum_col4(lsum);
       m_run[t] = m_new;
 
-      // O rows are nodes 4*grp+v; their rescale factor lives in lane 4*grp+v.
+      // O rows are nodes 4*grp+v; their rescale factors (one per node column)
+      // pass through this wave's 16 LDS floats: written by the lanes of
+      // group 0, read back as one 16-byte load (a wave's LDS accesses complete
+      // in order, so no barrier is needed; the merge's m slots are free until
+      // the walk ends).
+      if (grp == 0) sm_alpha[r16] = alpha;
+      __builtin_amdgcn_wave_barrier();
+      const float4 av4 = *(const float4*)(sm_alpha + grp * 4);
+      __builtin_amdgcn_wave_barrier();
+      const float av[4] = {av4.x, av4.y, av4.z, av4.w};
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float av = __shfl(alpha, grp * 4 + v);
+      for (int v = 0; v < 4; ++v)
 #pragma unroll
-        for (int n = 0; n < NO; ++n) O[t][n][v] *= av;
-      }
+        for (int n = 0; n < NO; ++n) O[t][n][v] *= av[v];
 
       if constexpr (sizeof(TK) == 2) {
         // A = P[node r16][tokens 4*grp..+3]; B = V[tokens 4*grp..+3][dim NO*r16 + n]
