@@ -88,19 +88,24 @@ constexpr size_t gemm_lds_cap() { return (MT == 1 || (MT <= 4 && NT <= 2)) ? 655
 
 // Cross-wave reduction in column passes of RC columns: the widest pass (a
 // multiple of 16 dividing the block's columns) for which the 8 waves'
-// partial tiles [8][ROWS][RC], the summed tile yfin [ROWS][COLS], the
+// partial tiles [8][ROWS][RC + pad], the summed tile yfin [ROWS][COLS], the
 // residual epilogue's squares aux [ROWS][COLS] and the row scales fit the
-// LDS cap, so every variant keeps 8 waves.
+// LDS cap, so every variant keeps 8 waves.  With several row tiles the rows
+// of the partial tiles are padded by 4 floats: a wave writes rows 4 apart
+// from its four 16-lane groups, which then fall on different LDS banks.
+template <int MT>
+constexpr int red_pad() { return MT >= 2 ? 4 : 0; }
 template <int MT, int NT>
 constexpr int red_cols() {
   for (int t = NT; t > 1; --t)
-    if (NT % t == 0 && (size_t)(8 * MT * 16 * (16 * t) + 2 * MT * 16 * NT * 16 + MT * 16) * 4 <= gemm_lds_cap<MT, NT>())
+    if (NT % t == 0 &&
+        (size_t)(8 * MT * 16 * (16 * t + red_pad<MT>()) + 2 * MT * 16 * NT * 16 + MT * 16) * 4 <= gemm_lds_cap<MT, NT>())
       return 16 * t;
   return 16;
 }
 template <int MT, int NT>
 constexpr size_t gemm_lds(int waves) {
-  return (size_t)(waves * MT * 16 * red_cols<MT, NT>() + 2 * MT * 16 * NT * 16 + MT * 16) * 4;
+  return (size_t)(waves * MT * 16 * (red_cols<MT, NT>() + red_pad<MT>()) + 2 * MT * 16 * NT * 16 + MT * 16) * 4;
 }
 
 // Epilogue operands of the one-row-tile residual epilogue (one output item
@@ -272,12 +277,14 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       if (i0 + D + j < n_my) compute(wv[j], xv[j]);
   }
 
-  // LDS: red[waves][ROWS][RC] | yfin[ROWS][COLS] | aux[ROWS][COLS] | rscale[ROWS].
-  // The waves' partial tiles meet in red one pass of RC columns at a time;
-  // their sum lands in yfin, the residual epilogue's squares in aux.
+  // LDS: red[waves][ROWS][RCP] | yfin[ROWS][COLS] | aux[ROWS][COLS] | rscale[ROWS].
+  // The waves' partial tiles meet in red one pass of RC columns at a time
+  // (rows RCP floats apart); their sum lands in yfin, the residual
+  // epilogue's squares in aux.
   constexpr int RC = red_cols<MT, NT>();
+  constexpr int RCP = RC + red_pad<MT>();
   float* red = smem;
-  float* yfin = red + waves * ROWS * RC;
+  float* yfin = red + waves * ROWS * RCP;
   float* aux = yfin + ROWS * COLS;
   float* rscale = aux + ROWS * COLS;
 
@@ -293,11 +300,48 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     if (lane == 0) rscale[wave] = rsqrtf(s / (float)a.norm_dim + a.eps);
   }
 
-  // When the row scale is known before the sums (loaded early, or no norm),
-  // it is applied as they are written (the same product as applying it
-  // afterwards), which saves a pass over the block and a barrier.  The
-  // residual projections (no norm, possibly K-split) always fold.
-  const bool fold = ss_early || !a.ss_in;
+  // With more rows than waves, the row scales come from eight threads per
+  // row, each summing a contiguous eighth of the row's partial sums (16-byte
+  // loads, all requested at once; then three exchanges, in a fixed order), in
+  // rounds of 64 rows.  The first round is requested before the waves'
+  // partial tiles go to LDS, so its latency overlaps those writes, and the
+  // scales are in LDS before the first pass sums.  (Row widths whose parts do
+  // not split into eighths of whole 16-byte loads take the path below.)
+  constexpr int kSsq = 16;  // 16-byte loads per thread: up to 512 parts per row
+  const bool ss_vec = MT >= 2 && a.ss_in && !ss_early && a.ss_nparts % 32 == 0 && a.ss_nparts <= 32 * kSsq &&
+                      a.ss_stride % 4 == 0;
+  const int nq4 = a.ss_nparts / 32;
+  float4 ssq[MT >= 2 ? kSsq : 1];
+  auto ss_load = [&](int r0) {
+    if constexpr (MT >= 2) {
+      const int row = min(r0 + ((int)threadIdx.x >> 3), M - 1);  // clamped: every thread loads
+      const float4* src = (const float4*)(a.ss_in + (size_t)row * a.ss_stride) + (threadIdx.x & 7) * nq4;
+#pragma unroll
+      for (int i = 0; i < kSsq; ++i)
+        if (i < nq4) ssq[i] = src[i];
+    }
+  };
+  auto ss_finish = [&](int r0) {
+    if constexpr (MT >= 2) {
+      float t = 0.f;
+#pragma unroll
+      for (int i = 0; i < kSsq; ++i)
+        if (i < nq4) t += (ssq[i].x + ssq[i].y) + (ssq[i].z + ssq[i].w);
+      t += __shfl_xor(t, 1);
+      t += __shfl_xor(t, 2);
+      t += __shfl_xor(t, 4);
+      const int row = r0 + ((int)threadIdx.x >> 3);
+      if ((threadIdx.x & 7) == 0 && row < M) rscale[row] = rsqrtf(t / (float)a.norm_dim + a.eps);
+    }
+  };
+  if (ss_vec) ss_load(0);
+
+  // When the row scale is known before the sums (loaded early or just above,
+  // or no norm), it is applied as they are written (the same product as
+  // applying it afterwards), which saves a pass over the block and a
+  // barrier.  The residual projections (no norm, possibly K-split) always
+  // fold.
+  const bool fold = ss_early || !a.ss_in || ss_vec;
 
   // MFMA result layout: lane holds column r16, rows 4*grp + v.
 #pragma unroll
@@ -309,12 +353,19 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       for (int nt = c0 / 16; nt < (c0 + RC) / 16; ++nt)
 #pragma unroll
         for (int v = 0; v < 4; ++v)
-          red[(wave * ROWS + mt * 16 + grp * 4 + v) * RC + nt * 16 - c0 + r16] = acc[mt][nt][v];
+          red[(wave * ROWS + mt * 16 + grp * 4 + v) * RCP + nt * 16 - c0 + r16] = acc[mt][nt][v];
+    if (c0 == 0 && ss_vec) {
+      ss_finish(0);
+      for (int r0 = (int)blockDim.x / 8; r0 < M; r0 += (int)blockDim.x / 8) {
+        ss_load(r0);
+        ss_finish(r0);
+      }
+    }
     __syncthreads();
     for (int e = threadIdx.x; e < M * RC; e += blockDim.x) {
       const int row = e / RC, col = e % RC;
       float s = 0.f;
-      for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * RC + col];
+      for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * RCP + col];
       yfin[row * COLS + c0 + col] = fold && a.ss_in ? s * rscale[row] : s;
     }
   }
