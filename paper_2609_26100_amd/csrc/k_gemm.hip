@@ -370,6 +370,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     }
   }
 
+  bool split_done = false;  // the K-split merge ran the residual epilogue's element-wise part
   if (SPLIT && ks > 1) {
     // K split: publish this workgroup's sums (agent-scope stores: visible to
     // every XCD once acknowledged), count the arrival, and let the last
@@ -391,21 +392,48 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       s_last = __hip_atomic_fetch_add(a.kcount + strip, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ks - 1;
     __syncthreads();
     if (!s_last) return;
-    for (int e4 = threadIdx.x; e4 < M * COLS / 4; e4 += blockDim.x) {
-      f4v v[kMaxKSplit];
+    // The last arrival adds the partial tiles and runs the residual
+    // epilogue's element-wise part on the sums directly, two elements per
+    // thread at a time, with all their requests (the other splits' partial
+    // tiles, h, the next norm's gain) issued together.
+    const int N = a.N, n4 = M * COLS / 4;
+    for (int b0 = threadIdx.x; b0 < n4; b0 += 2 * (int)blockDim.x) {
+      f4v v[2][kMaxKSplit];
+      float4 h0[2], gn[2];
 #pragma unroll
-      for (int k = 0; k < kMaxKSplit; ++k)
-        if (k < ks && k != split)
-          v[k] = __builtin_amdgcn_raw_buffer_load_b128(
-              pres, (int)(((size_t)(strip * ks + k) * slot_floats + 4 * e4) * sizeof(float)), 0, kScopeAgent);
-      const f4v own = *(const f4v*)(yfin + 4 * e4);
-      f4v t = {0.f, 0.f, 0.f, 0.f};
+      for (int u = 0; u < 2; ++u) {
+        const int e4 = min(b0 + u * (int)blockDim.x, n4 - 1);  // clamped: every thread loads
+        const int row = e4 / (COLS / 4), col = (e4 % (COLS / 4)) * 4;
 #pragma unroll
-      for (int k = 0; k < kMaxKSplit; ++k)
-        if (k < ks) t += k == split ? own : v[k];
-      *(f4v*)(yfin + 4 * e4) = t;
+        for (int k = 0; k < kMaxKSplit; ++k)
+          if (k < ks && k != split)
+            v[u][k] = __builtin_amdgcn_raw_buffer_load_b128(
+                pres, (int)(((size_t)(strip * ks + k) * slot_floats + 4 * e4) * sizeof(float)), 0, kScopeAgent);
+        h0[u] = *(const float4*)(a.h + (size_t)row * N + strip * COLS + col);
+        gn[u] = *(const float4*)(a.g_next[s_seq[row]] + strip * COLS + col);
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int e4 = b0 + u * (int)blockDim.x;
+        if (e4 >= n4) break;
+        const int row = e4 / (COLS / 4), col = (e4 % (COLS / 4)) * 4;
+        const f4v own = *(const f4v*)(yfin + 4 * e4);
+        f4v t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < kMaxKSplit; ++k)
+          if (k < ks) t += k == split ? own : v[u][k];
+        // rows whose sequence skips this block keep h, their next-norm input
+        // and their partial sums untouched
+        if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
+        const float4 hn = make_float4(h0[u].x + t.x, h0[u].y + t.y, h0[u].z + t.z, h0[u].w + t.w);
+        *(float4*)(a.h + (size_t)row * N + strip * COLS + col) = hn;
+        store_act4<T>(a.xn, a.xn_plane, act_index<T>(row, strip * COLS + col, N),
+                      make_float4(hn.x * gn[u].x, hn.y * gn[u].y, hn.z * gn[u].z, hn.w * gn[u].w));
+        *(float4*)(aux + row * COLS + col) = make_float4(hn.x * hn.x, hn.y * hn.y, hn.z * hn.z, hn.w * hn.w);
+      }
     }
     if (threadIdx.x == 0) a.kcount[strip] = 0;
+    split_done = true;
   }
 
   if (!fold) {
@@ -477,7 +505,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     // four adjacent columns per thread: vector loads and stores of h, the
     // gain and the next-norm input (adjacent in each activation plane)
     const int N = a.N;
-    for (int e4 = threadIdx.x; e4 < M * COLS / 4; e4 += blockDim.x) {
+    for (int e4 = threadIdx.x; e4 < (split_done ? 0 : M * COLS / 4); e4 += blockDim.x) {
       const int row = e4 / (COLS / 4), col = (e4 % (COLS / 4)) * 4;
       if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
       const size_t idx = (size_t)row * N + n0 + col;
