@@ -124,6 +124,17 @@ __device__ __forceinline__ void prefetch_epilogue(const GemmArgs& a, int M, int 
   }
 }
 
+// Row r's segment runs this block: bit r of the two row_on words, read as
+// uniform values (scalar loads) with the bit selected per lane.  (Indexing
+// the argument block per lane instead makes a vector load from it, whose wait
+// sits in every epilogue iteration.)
+static_assert(kMaxRows == 128, "two words of row bits");
+struct RowBits {
+  uint64_t w0, w1;
+  __device__ __forceinline__ explicit RowBits(const GemmArgs& a) : w0(a.row_on[0]), w1(a.row_on[1]) {}
+  __device__ __forceinline__ bool on(int r) const { return ((r < 64 ? w0 : w1) >> (r & 63)) & 1ull; }
+};
+
 template <typename T, int MT, int NT, int EPI>
 __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
@@ -178,6 +189,8 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   __shared__ int s_seq[EPI == EPI_QKV || EPI == EPI_RESID ? kMaxRows : 1];
   __shared__ int s_slot[EPI == EPI_QKV ? kMaxRows : 1];
   __shared__ int s_pos[EPI == EPI_QKV ? kMaxRows : 1];
+  __shared__ int s_page[EPI == EPI_QKV ? kMaxRows : 1];                // KV page of the row's slot
+  __shared__ const float* s_gain[EPI == EPI_RESID ? kMaxRows : 1];    // next-norm gain of the row's segment
   if constexpr (EPI == EPI_QKV || EPI == EPI_RESID) {
     for (int r = threadIdx.x; r < M; r += blockDim.x) {
       const int sq = a.n_seqs == 1 ? 0 : a.sp->row_seq[r];
@@ -275,6 +288,22 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < D; ++j)
       if (i0 + D + j < n_my) compute(wv[j], xv[j]);
+  }
+
+  // Per-row lookups of the epilogue that depend on the prologue's row data
+  // (each thread reads the rows it wrote there), requested now so they land
+  // while the waves' partial tiles are reduced; the reduction's barriers
+  // publish them.
+  const RowBits rows(a);
+  if constexpr (EPI == EPI_QKV) {
+    for (int r = threadIdx.x; r < M; r += blockDim.x) {
+      const int lp = s_slot[r] >> 4;
+      if (rows.on(r)) s_page[r] = lp < a.n_arg_pages ? a.pages[lp] : a.page_table[a.pt_off[s_seq[r]] + lp];
+    }
+  }
+  if constexpr (EPI == EPI_RESID) {
+    if (a.n_seqs > 1)
+      for (int r = threadIdx.x; r < M; r += blockDim.x) s_gain[r] = a.g_next[s_seq[r]];
   }
 
   // LDS: red[waves][ROWS][RCP] | yfin[ROWS][COLS] | aux[ROWS][COLS] | rscale[ROWS].
@@ -410,7 +439,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
             v[u][k] = __builtin_amdgcn_raw_buffer_load_b128(
                 pres, (int)(((size_t)(strip * ks + k) * slot_floats + 4 * e4) * sizeof(float)), 0, kScopeAgent);
         h0[u] = *(const float4*)(a.h + (size_t)row * N + strip * COLS + col);
-        gn[u] = *(const float4*)(a.g_next[s_seq[row]] + strip * COLS + col);
+        gn[u] = *(const float4*)((a.n_seqs == 1 ? a.g_next[0] : s_gain[row]) + strip * COLS + col);
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -424,7 +453,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
           if (k < ks) t += k == split ? own : v[u][k];
         // rows whose sequence skips this block keep h, their next-norm input
         // and their partial sums untouched
-        if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
+        if (!rows.on(row)) continue;
         const float4 hn = make_float4(h0[u].x + t.x, h0[u].y + t.y, h0[u].z + t.z, h0[u].w + t.w);
         *(float4*)(a.h + (size_t)row * N + strip * COLS + col) = hn;
         store_act4<T>(a.xn, a.xn_plane, act_index<T>(row, strip * COLS + col, N),
@@ -470,33 +499,52 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   if constexpr (EPI == EPI_QKV) {
     const int HD = a.head_dim, d = a.d;
     const int d16 = d >> 4, hd16 = HD >> 4;
-    for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
-      const int row = e / COLS, col = e % COLS;
-      const int n = n0 + col;
-      const int tile = n >> 4, c = n & 15;
-      const int sec = tile / d16, ts = tile % d16;
-      const int head = ts / hd16, t = ts % hd16;
-      const int dim = c < 8 ? 8 * t + c : (HD >> 1) + 8 * t + (c - 8);
-      float val = yfin[row * COLS + col];
-      if (sec < 2) {
-        const float partner = yfin[row * COLS + (col ^ 8)];
-        const float2 cs = a.rope[(size_t)s_pos[row] * (HD >> 1) + 8 * t + (c & 7)];
-        val = c < 8 ? val * cs.x - partner * cs.y : val * cs.x + partner * cs.y;
+    // Elements in batches of QB per thread (what the launch gives a thread
+    // with 8 waves, at most 8): the batch's rotary coefficients are requested
+    // together before any of its stores, so they cost one round trip.
+    constexpr int QB = (ROWS * COLS + 511) / 512 > 8 ? 8 : (ROWS * COLS + 511) / 512;
+    for (int e0 = threadIdx.x; e0 < M * COLS; e0 += QB * (int)blockDim.x) {
+      float2 cs[QB];
+      int sec[QB], head[QB], dim[QB];
+#pragma unroll
+      for (int j = 0; j < QB; ++j) {
+        const int e = e0 + j * (int)blockDim.x;
+        if (e < M * COLS) {
+          const int row = e / COLS, col = e % COLS;
+          const int n = n0 + col;
+          const int tile = n >> 4, c = n & 15;
+          sec[j] = tile / d16;
+          const int ts = tile % d16;
+          head[j] = ts / hd16;
+          const int t = ts % hd16;
+          dim[j] = c < 8 ? 8 * t + c : (HD >> 1) + 8 * t + (c - 8);
+          // every column has a rotary index (< hd / 2), so the request is in
+          // bounds even where the value goes unused (v)
+          cs[j] = a.rope[(size_t)s_pos[row] * (HD >> 1) + 8 * t + (c & 7)];
+        }
       }
-      if (sec == 0) {
-        a.q[(size_t)row * d + head * HD + dim] = val;
-      } else if ((a.row_on[row >> 6] >> (row & 63)) & 1ull) {
-        const int sq = s_seq[row];
-        const int slot = s_slot[row];
-        const int lp = slot >> 4;
-        const int page = lp < a.n_arg_pages ? a.pages[lp] : a.page_table[a.pt_off[sq] + lp];
-        const int tin = slot & 15;
-        KV* blk = (KV*)a.kv_pages +
-                  ((((size_t)a.layer * a.n_pages_pool + page) * 2 + (sec - 1)) * a.n_heads + head) * (16 * (size_t)HD);
-        if (sec == 1)
-          blk[tin * HD + dim] = (KV)val;
-        else
-          blk[(tin >> 2) * HD * 4 + dim * 4 + (tin & 3)] = (KV)val;
+#pragma unroll
+      for (int j = 0; j < QB; ++j) {
+        const int e = e0 + j * (int)blockDim.x;
+        if (e >= M * COLS) break;
+        const int row = e / COLS, col = e % COLS, c = col & 15;
+        float val = yfin[row * COLS + col];
+        if (sec[j] < 2) {
+          const float partner = yfin[row * COLS + (col ^ 8)];
+          val = c < 8 ? val * cs[j].x - partner * cs[j].y : val * cs[j].x + partner * cs[j].y;
+        }
+        if (sec[j] == 0) {
+          a.q[(size_t)row * d + head[j] * HD + dim[j]] = val;
+        } else if (rows.on(row)) {
+          const int tin = s_slot[row] & 15;
+          KV* blk = (KV*)a.kv_pages +
+                    ((((size_t)a.layer * a.n_pages_pool + s_page[row]) * 2 + (sec[j] - 1)) * a.n_heads + head[j]) *
+                        (16 * (size_t)HD);
+          if (sec[j] == 1)
+            blk[tin * HD + dim[j]] = (KV)val;
+          else
+            blk[(tin >> 2) * HD * 4 + dim[j] * 4 + (tin & 3)] = (KV)val;
+        }
       }
     }
   } else if constexpr (EPI == EPI_RESID) {
@@ -507,7 +555,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     const int N = a.N;
     for (int e4 = threadIdx.x; e4 < (split_done ? 0 : M * COLS / 4); e4 += blockDim.x) {
       const int row = e4 / (COLS / 4), col = (e4 % (COLS / 4)) * 4;
-      if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
+      if (!rows.on(row)) continue;
       const size_t idx = (size_t)row * N + n0 + col;
       // one pass (always with one row tile): the operands prefetched for e4
       const bool pre = PRE_RESID && M * COLS / 4 <= (int)blockDim.x && n_my > 0;
@@ -522,7 +570,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       if (pre && a.n_seqs == 1)
         gn = pre_g;
       else
-        gn = *(const float4*)(a.g_next[s_seq[row]] + n0 + col);
+        gn = *(const float4*)((a.n_seqs == 1 ? a.g_next[0] : s_gain[row]) + n0 + col);
       store_act4<T>(a.xn, a.xn_plane, act_index<T>(row, n0 + col, N),
                     make_float4(hn.x * gn.x, hn.y * gn.y, hn.z * gn.z, hn.w * gn.w));
       *(float4*)(aux + row * COLS + col) = make_float4(hn.x * hn.x, hn.y * hn.y, hn.z * hn.z, hn.w * hn.w);
@@ -531,7 +579,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     // one partial sum of h^2 per 16 columns (the format every norm reads)
     for (int e = threadIdx.x; e < M * NT; e += blockDim.x) {
       const int row = e / NT, j = e % NT;
-      if (!((a.row_on[row >> 6] >> (row & 63)) & 1ull)) continue;
+      if (!rows.on(row)) continue;
       float s = 0.f;
       for (int col = j * 16; col < j * 16 + 16; ++col) s += aux[row * COLS + col];
       a.ss_out[(size_t)row * a.ss_stride + strip * NT + j] = s;
