@@ -93,19 +93,28 @@ constexpr size_t gemm_lds_cap() { return (MT == 1 || (MT <= 4 && NT <= 2)) ? 655
 // LDS cap, so every variant keeps 8 waves.  With several row tiles the rows
 // of the partial tiles are padded by 4 floats: a wave writes rows 4 apart
 // from its four 16-lane groups, which then fall on different LDS banks.
+// With several row tiles the gate/up passes apply SwiGLU and store straight
+// from the partial tiles (whole gate/up pairs per pass), so that block keeps
+// neither yfin nor aux and its passes can be wider.
 template <int MT>
 constexpr int red_pad() { return MT >= 2 ? 4 : 0; }
-template <int MT, int NT>
+template <int MT, int EPI>
+constexpr bool fused_epi() { return EPI == EPI_SWIGLU && MT >= 2; }
+template <int MT, int NT, int EPI>
+constexpr size_t gemm_lds_floats(int waves, int rc) {
+  return (size_t)waves * MT * 16 * (rc + red_pad<MT>()) + (fused_epi<MT, EPI>() ? 0 : 2 * MT * 16 * NT * 16) + MT * 16;
+}
+template <int MT, int NT, int EPI>
 constexpr int red_cols() {
   for (int t = NT; t > 1; --t)
-    if (NT % t == 0 &&
-        (size_t)(8 * MT * 16 * (16 * t + red_pad<MT>()) + 2 * MT * 16 * NT * 16 + MT * 16) * 4 <= gemm_lds_cap<MT, NT>())
+    if (NT % t == 0 && (!fused_epi<MT, EPI>() || t % 2 == 0) &&
+        gemm_lds_floats<MT, NT, EPI>(8, 16 * t) * 4 <= gemm_lds_cap<MT, NT>())
       return 16 * t;
-  return 16;
+  return fused_epi<MT, EPI>() ? 32 : 16;
 }
-template <int MT, int NT>
+template <int MT, int NT, int EPI>
 constexpr size_t gemm_lds(int waves) {
-  return (size_t)(waves * MT * 16 * (red_cols<MT, NT>() + red_pad<MT>()) + 2 * MT * 16 * NT * 16 + MT * 16) * 4;
+  return gemm_lds_floats<MT, NT, EPI>(waves, red_cols<MT, NT, EPI>()) * 4;
 }
 
 // Epilogue operands of the one-row-tile residual epilogue (one output item
@@ -306,16 +315,17 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       for (int r = threadIdx.x; r < M; r += blockDim.x) s_gain[r] = a.g_next[s_seq[r]];
   }
 
-  // LDS: red[waves][ROWS][RCP] | yfin[ROWS][COLS] | aux[ROWS][COLS] | rscale[ROWS].
-  // The waves' partial tiles meet in red one pass of RC columns at a time
-  // (rows RCP floats apart); their sum lands in yfin, the residual
-  // epilogue's squares in aux.
-  constexpr int RC = red_cols<MT, NT>();
+  // LDS: red[waves][ROWS][RCP] | yfin[ROWS][COLS] | aux[ROWS][COLS] | rscale[ROWS]
+  // (gate/up with several row tiles: red | rscale).  The waves' partial tiles
+  // meet in red one pass of RC columns at a time (rows RCP floats apart);
+  // their sum lands in yfin, the residual epilogue's squares in aux.
+  constexpr bool FUSED = fused_epi<MT, EPI>();
+  constexpr int RC = red_cols<MT, NT, EPI>();
   constexpr int RCP = RC + red_pad<MT>();
   float* red = smem;
   float* yfin = red + waves * ROWS * RCP;
-  float* aux = yfin + ROWS * COLS;
-  float* rscale = aux + ROWS * COLS;
+  float* aux = yfin + (FUSED ? 0 : ROWS * COLS);
+  float* rscale = aux + (FUSED ? 0 : ROWS * COLS);
 
   // RMSNorm row scale from the producer's partial sums (fixed order, so every
   // workgroup derives the same value): here when each row has its own wave
@@ -329,33 +339,43 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     if (lane == 0) rscale[wave] = rsqrtf(s / (float)a.norm_dim + a.eps);
   }
 
-  // With more rows than waves, the row scales come from eight threads per
-  // row, each summing a contiguous eighth of the row's partial sums (16-byte
-  // loads, all requested at once; then three exchanges, in a fixed order), in
-  // rounds of 64 rows.  The first round is requested before the waves'
-  // partial tiles go to LDS, so its latency overlaps those writes, and the
-  // scales are in LDS before the first pass sums.  (Row widths whose parts do
-  // not split into eighths of whole 16-byte loads take the path below.)
-  constexpr int kSsq = 16;  // 16-byte loads per thread: up to 512 parts per row
-  const bool ss_vec = MT >= 2 && a.ss_in && !ss_early && a.ss_nparts % 32 == 0 && a.ss_nparts <= 32 * kSsq &&
-                      a.ss_stride % 4 == 0;
-  const int nq4 = a.ss_nparts / 32;
+  // With several row tiles, the row scales come from eight threads per row,
+  // each summing a contiguous eighth of the row's partial sums, then three
+  // exchanges (a fixed order), in rounds of 64 rows.  Where the row splits
+  // into eighths of whole 16-byte groups, the groups are requested before the
+  // waves' partial tiles go to LDS, so their latency overlaps those writes;
+  // other row widths (small models) load and add their parts one by one,
+  // the parts past the row counting as zero.  Either way the scales are in
+  // LDS before the first pass sums.
+  constexpr int kSsq = 16;  // groups of four parts per thread: up to 512 parts per row
+  const bool ss_vec = MT >= 2 && a.ss_in;
+  const int nq4 = (a.ss_nparts + 31) / 32;
+  const bool ss_wide = a.ss_nparts % 32 == 0 && a.ss_stride % 4 == 0;  // 16-byte loads
   float4 ssq[MT >= 2 ? kSsq : 1];
   auto ss_load = [&](int r0) {
     if constexpr (MT >= 2) {
       const int row = min(r0 + ((int)threadIdx.x >> 3), M - 1);  // clamped: every thread loads
-      const float4* src = (const float4*)(a.ss_in + (size_t)row * a.ss_stride) + (threadIdx.x & 7) * nq4;
+      const float* src = a.ss_in + (size_t)row * a.ss_stride + (threadIdx.x & 7) * nq4 * 4;
+      if (ss_wide) {
 #pragma unroll
-      for (int i = 0; i < kSsq; ++i)
-        if (i < nq4) ssq[i] = src[i];
+        for (int i = 0; i < kSsq; ++i)
+          if (i < nq4) ssq[i] = *(const float4*)(src + 4 * i);
+      }
     }
   };
   auto ss_finish = [&](int r0) {
     if constexpr (MT >= 2) {
       float t = 0.f;
+      if (ss_wide) {
 #pragma unroll
-      for (int i = 0; i < kSsq; ++i)
-        if (i < nq4) t += (ssq[i].x + ssq[i].y) + (ssq[i].z + ssq[i].w);
+        for (int i = 0; i < kSsq; ++i)
+          if (i < nq4) t += (ssq[i].x + ssq[i].y) + (ssq[i].z + ssq[i].w);
+      } else {
+        const int row = min(r0 + ((int)threadIdx.x >> 3), M - 1);
+        const int p0 = (threadIdx.x & 7) * nq4 * 4;
+        const float* src = a.ss_in + (size_t)row * a.ss_stride;
+        for (int q = p0; q < p0 + nq4 * 4; ++q) t += q < a.ss_nparts ? src[q] : 0.f;
+      }
       t += __shfl_xor(t, 1);
       t += __shfl_xor(t, 2);
       t += __shfl_xor(t, 4);
@@ -391,11 +411,37 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       }
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < M * RC; e += blockDim.x) {
-      const int row = e / RC, col = e % RC;
-      float s = 0.f;
-      for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * RCP + col];
-      yfin[row * COLS + c0 + col] = fold && a.ss_in ? s * rscale[row] : s;
+    if constexpr (FUSED) {
+      // gate/up: four adjacent outputs of a pair per thread, gate and up
+      // summed in wave order, scaled, silu(gate) * up, one vector store per
+      // plane (the same operations as summing into yfin first)
+      constexpr int PP = RC / 32;  // gate/up pairs per pass
+      const int F = a.N >> 1;
+      for (int it = threadIdx.x; it < M * PP * 4; it += blockDim.x) {
+        const int row = it / (PP * 4), jp = (it >> 2) % PP, c = (it & 3) * 4;
+        const float* rg = red + row * RCP + jp * 32 + c;
+        float4 g = make_float4(0.f, 0.f, 0.f, 0.f), u = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int w = 0; w < waves; ++w) {
+          const float4 gw = *(const float4*)(rg + w * ROWS * RCP);
+          const float4 uw = *(const float4*)(rg + w * ROWS * RCP + 16);
+          g.x += gw.x; g.y += gw.y; g.z += gw.z; g.w += gw.w;
+          u.x += uw.x; u.y += uw.y; u.z += uw.z; u.w += uw.w;
+        }
+        if (a.ss_in) {
+          const float r = rscale[row];
+          g = make_float4(g.x * r, g.y * r, g.z * r, g.w * r);
+          u = make_float4(u.x * r, u.y * r, u.z * r, u.w * r);
+        }
+        store_act4<T>(a.act, a.act_plane, act_index<T>(row, (strip * (NT / 2) + c0 / 32 + jp) * 16 + c, F),
+                      make_float4(silu(g.x) * u.x, silu(g.y) * u.y, silu(g.z) * u.z, silu(g.w) * u.w));
+      }
+    } else {
+      for (int e = threadIdx.x; e < M * RC; e += blockDim.x) {
+        const int row = e / RC, col = e % RC;
+        float s = 0.f;
+        for (int w = 0; w < waves; ++w) s += red[(w * ROWS + row) * RCP + col];
+        yfin[row * COLS + c0 + col] = fold && a.ss_in ? s * rscale[row] : s;
+      }
     }
   }
 
@@ -493,7 +539,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
     __syncthreads();
     for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) yfin[e] *= rscale[e / COLS];
   }
-  __syncthreads();
+  if constexpr (!FUSED) __syncthreads();
 
   const int n0 = strip * COLS;
   if constexpr (EPI == EPI_QKV) {
@@ -584,7 +630,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       for (int col = j * 16; col < j * 16 + 16; ++col) s += aux[row * COLS + col];
       a.ss_out[(size_t)row * a.ss_stride + strip * NT + j] = s;
     }
-  } else if constexpr (EPI == EPI_SWIGLU) {
+  } else if constexpr (EPI == EPI_SWIGLU && !FUSED) {
     static_assert(NT % 2 == 0, "gate and up tiles pair up");
     const int F = a.N >> 1;
     constexpr int PAIRS = NT / 2;
@@ -596,7 +642,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       store_act4<T>(a.act, a.act_plane, act_index<T>(row, (strip * PAIRS + j) * 16 + c, F),
                     make_float4(silu(g[0]) * u[0], silu(g[1]) * u[1], silu(g[2]) * u[2], silu(g[3]) * u[3]));
     }
-  } else {  // EPI_LOGITS
+  } else if constexpr (EPI == EPI_LOGITS) {
     const int N = a.N;
     for (int e = threadIdx.x; e < M * COLS; e += blockDim.x) {
       const int row = e / COLS, col = e % COLS;
@@ -675,8 +721,8 @@ static hipError_t launch_v(const GemmArgs& a, hipStream_t s) {
   const size_t cap = gemm_lds_cap<MT, NT>();
   const int nkc_min = a.nkc / a.ksplit;  // chunks of the smallest K split
   int waves = nkc_min < 8 ? nkc_min : 8;
-  while (waves > 1 && gemm_lds<MT, NT>(waves) > cap) waves >>= 1;
-  const size_t lds = gemm_lds<MT, NT>(waves);
+  while (waves > 1 && gemm_lds<MT, NT, EPI>(waves) > cap) waves >>= 1;
+  const size_t lds = gemm_lds<MT, NT, EPI>(waves);
   dim3 grid(a.N / (16 * NT) * a.ksplit), block(waves * 64);
   TSS_LAUNCH((k_gemm<T, MT, NT, EPI>), grid, block, lds, s, a);
   return hipGetLastError();
