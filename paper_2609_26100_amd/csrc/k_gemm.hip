@@ -144,8 +144,11 @@ struct RowBits {
   __device__ __forceinline__ bool on(int r) const { return ((r < 64 ? w0 : w1) >> (r & 63)) & 1ull; }
 };
 
-template <typename T, int MT, int NT, int EPI>
-__global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
+// The workgroup's projection: its strip (blockIdx.x, with a K split
+// blockIdx.x / ksplit); for gate/up its NT / 2 pairs from strip * NT / 2 on,
+// or from pair0 on in launches of two block widths (GIVEN).
+template <typename T, int MT, int NT, int EPI, bool GIVEN = false>
+__device__ __forceinline__ void gemm_body(GemmArgs a, int pair0 = 0) {
   constexpr int KC = 64 / sizeof(T);   // K elements per 1 KiB tile
   constexpr int KL = KC / 4;           // K elements per lane per tile
   constexpr int S = Mode<T>::planes;
@@ -170,6 +173,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   const int strip = SPLIT ? (int)blockIdx.x / ks : (int)blockIdx.x;
   const int split = SPLIT ? (int)blockIdx.x - strip * ks : 0;
   const int c_lo = SPLIT ? split * nkc / ks : 0, c_hi = SPLIT ? (split + 1) * nkc / ks : nkc;
+  if constexpr (!GIVEN) pair0 = strip * (NT / 2);
   // weight tile nt of this strip, chunk c, at wb[nt] + c * wstep: plain
   // matrices store a 16-row tile's chunks consecutively; gate and up tiles of
   // one pair alternate chunk by chunk
@@ -178,7 +182,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
   if constexpr (EPI == EPI_SWIGLU) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
-      wb[nt] = a.w + (((size_t)(strip * (NT / 2) + nt / 2) * nkc * 2) + (nt & 1)) * kTileBytes + lane * 16;
+      wb[nt] = a.w + (((size_t)(pair0 + nt / 2) * nkc * 2) + (nt & 1)) * kTileBytes + lane * 16;
     wstep = 2 * kTileBytes;
   } else {
 #pragma unroll
@@ -432,7 +436,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
           g = make_float4(g.x * r, g.y * r, g.z * r, g.w * r);
           u = make_float4(u.x * r, u.y * r, u.z * r, u.w * r);
         }
-        store_act4<T>(a.act, a.act_plane, act_index<T>(row, (strip * (NT / 2) + c0 / 32 + jp) * 16 + c, F),
+        store_act4<T>(a.act, a.act_plane, act_index<T>(row, (pair0 + c0 / 32 + jp) * 16 + c, F),
                       make_float4(silu(g.x) * u.x, silu(g.y) * u.y, silu(g.z) * u.z, silu(g.w) * u.w));
       }
     } else {
@@ -639,7 +643,7 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
       const int row = e4 / (4 * PAIRS), j = (e4 / 4) % PAIRS, c = (e4 & 3) * 4;
       const float* g = yfin + row * COLS + j * 32 + c;
       const float* u = g + 16;
-      store_act4<T>(a.act, a.act_plane, act_index<T>(row, (strip * PAIRS + j) * 16 + c, F),
+      store_act4<T>(a.act, a.act_plane, act_index<T>(row, (pair0 + j) * 16 + c, F),
                     make_float4(silu(g[0]) * u[0], silu(g[1]) * u[1], silu(g[2]) * u[2], silu(g[3]) * u[3]));
     }
   } else if constexpr (EPI == EPI_LOGITS) {
@@ -666,6 +670,25 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
 
 
 template <typename T, int MT, int NT, int EPI>
+__global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
+  gemm_body<T, MT, NT, EPI>(a);
+}
+
+// Gate/up in exactly one round of 256 workgroups where the pairs do not
+// divide into equal blocks that fill it: workgroups [0, wide_wgs) take
+// NT / 2 pairs, the rest NT / 2 - 1 (7B with 2-4 row tiles: 176 x 3 + 80 x 2
+// = 688 pairs, instead of 172 blocks of 4 pairs that leave 84 CUs idle
+// while each busy CU streams 1.5 MiB).
+template <typename T, int MT, int NT>
+__global__ __launch_bounds__(512) void k_gemm_gu2(GemmArgs a) {
+  const int b = blockIdx.x;
+  if (b < a.wide_wgs)
+    gemm_body<T, MT, NT, EPI_SWIGLU, true>(a, b * (NT / 2));
+  else
+    gemm_body<T, MT, NT - 2, EPI_SWIGLU, true>(a, a.wide_wgs * (NT / 2) + (b - a.wide_wgs) * (NT / 2 - 1));
+}
+
+template <typename T, int MT, int NT, int EPI>
 static hipError_t gemm_attr() {
   return hipFuncSetAttribute((const void*)k_gemm<T, MT, NT, EPI>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)kGemmLdsMax);
@@ -690,6 +713,10 @@ static hipError_t gemm_attr_rows() {
   if (e == hipSuccess) e = gemm_attr<T, MT, 3, EPI_QKV>();  // three-tile blocks: Q/K/V only
   if constexpr (MT >= 2 && MT <= 4)  // eight-tile gate/up blocks (four pairs)
     if (e == hipSuccess) e = gemm_attr<T, MT, 8, EPI_SWIGLU>();
+  if constexpr (MT >= 2 && MT <= 4)  // gate/up blocks of three and two pairs
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void*)k_gemm_gu2<T, MT, 6>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)kGemmLdsMax);
   if constexpr (MT >= 2 && MT <= 4)  // six-tile Q/K/V blocks
     if (e == hipSuccess) e = gemm_attr<T, MT, 6, EPI_QKV>();
   if constexpr (MT >= 2 && MT <= 3)  // ten-tile gate/up blocks (five pairs)
@@ -728,6 +755,19 @@ static hipError_t launch_v(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <typename T, int MT>
+static hipError_t launch_gu2(const GemmArgs& a, hipStream_t s) {
+  const int nkc_min = a.nkc;
+  int waves = nkc_min < 8 ? nkc_min : 8;
+  auto lds_of = [](int w) {
+    const size_t l6 = gemm_lds<MT, 6, EPI_SWIGLU>(w), l4 = gemm_lds<MT, 4, EPI_SWIGLU>(w);
+    return l6 > l4 ? l6 : l4;
+  };
+  while (waves > 1 && lds_of(waves) > gemm_lds_cap<MT, 6>()) waves >>= 1;
+  TSS_LAUNCH((k_gemm_gu2<T, MT, 6>), dim3(kGemmRound), dim3(waves * 64), lds_of(waves), s, a);
+  return hipGetLastError();
+}
+
 template <typename T, int MT, int NT>
 static hipError_t launch_mt(int epi, const GemmArgs& a, hipStream_t s) {
   switch (epi) {
@@ -751,7 +791,10 @@ static hipError_t launch_rows(int epi, int nt, const GemmArgs& a, hipStream_t s)
       if constexpr (MT >= 2 && MT <= 4) return epi == EPI_SWIGLU ? launch_v<T, MT, 8, EPI_SWIGLU>(a, s) : hipErrorInvalidValue;
       return hipErrorInvalidValue;
     case 6:
-      if constexpr (MT >= 2 && MT <= 4) return epi == EPI_QKV ? launch_v<T, MT, 6, EPI_QKV>(a, s) : hipErrorInvalidValue;
+      if constexpr (MT >= 2 && MT <= 4) {
+        if (epi == EPI_QKV) return launch_v<T, MT, 6, EPI_QKV>(a, s);
+        if (epi == EPI_SWIGLU && a.wide_wgs > 0) return launch_gu2<T, MT>(a, s);
+      }
       return hipErrorInvalidValue;
     case 10:
       if constexpr (MT >= 2 && MT <= 3) return epi == EPI_SWIGLU ? launch_v<T, MT, 10, EPI_SWIGLU>(a, s) : hipErrorInvalidValue;
@@ -761,7 +804,7 @@ static hipError_t launch_rows(int epi, int nt, const GemmArgs& a, hipStream_t s)
 }
 
 hipError_t launch_gemm(bool bf16, int epi, int mt, int nt, const GemmArgs& a, hipStream_t s) {
-  if (nt != gemm_tiles(epi, mt, a.N)) return hipErrorInvalidValue;
+  if (nt != gemm_tiles(epi, mt, a.N) || a.wide_wgs != gemm_wide_wgs(epi, mt, a.N)) return hipErrorInvalidValue;
   if (a.ksplit != gemm_ksplit(epi, mt, a.N, a.nkc) || (a.ksplit > 1 && (!a.kpart || !a.kcount)))
     return hipErrorInvalidValue;
   if (bf16) {

@@ -852,6 +852,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
   base.ss_nparts = d / 16;
   base.am_stride = cf.vocab / 16;
   base.ksplit = 1;
+  base.wide_wgs = 0;
   base.sp = sp_dev;
   base.row_on[0] = base.row_on[1] = ~0ull;
 
@@ -983,6 +984,7 @@ int enqueue_step(tss_ctx* c, bool verify, hipStream_t s, int start_layer = 0, co
       a.ss_in = (const float*)(ws + c->wsl.ss_m);
       a.act = ws + c->wsl.act;
       a.act_plane = plane_f;
+      a.wide_wgs = gemm_wide_wgs(EPI_SWIGLU, mt, a.N);
       ProfScope ps(c, TSS_K_GATEUP, l);
       HIPCHK(launch_gemm(c->bf16, EPI_SWIGLU, mt, gemm_tiles(EPI_SWIGLU, mt, a.N), a, s), "gate/up gemm");
       ps.done();

@@ -184,6 +184,9 @@ struct GemmArgs {
   // its share of K; the ksplit partial products of a strip meet in kpart
   // (agent-scope accesses) and the last workgroup to arrive finishes the strip
   int ksplit;
+  // gate/up in blocks of two widths (gemm_wide_wgs > 0): workgroups
+  // [0, wide_wgs) take NT / 2 pairs, the rest NT / 2 - 1
+  int wide_wgs;
   float* kpart;            // [strips * ksplit][Mp][16 * NT] partial products
   int* kcount;             // [strips] arrivals, zero between launches
   const StepParams* sp;
@@ -351,7 +354,22 @@ int verify_in_workspace(tss_ctx* c, uint8_t* base, int32_t seq, const int32_t* t
 // The residual projections with 2-8 row tiles take four- (two-) tile blocks
 // over a share of K instead (gemm_ksplit; the partial tiles meet through agent-scope
 // accesses, with no device-scope fence).
+// Workgroups of one projection round on this GPU (one per CU).
+constexpr int kGemmRound = 256;
+
+// Gate/up with 2-4 row tiles whose pairs (N / 32) lie between two and three
+// per workgroup of a 256-workgroup round: blocks of three pairs (six tiles)
+// for the first `pairs - 512` workgroups and of two for the rest, so every
+// CU streams (7B: 176 x 3 + 80 x 2 pairs instead of 172 x 4).  Returns that
+// count of three-pair workgroups, or 0.
+inline int gemm_wide_wgs(int epi, int mt, int N) {
+  if (epi != EPI_SWIGLU || mt < 2 || mt > 4 || N % 32) return 0;
+  const int pairs = N / 32;
+  return pairs > 2 * kGemmRound && pairs <= 3 * kGemmRound ? pairs - 2 * kGemmRound : 0;
+}
+
 inline int gemm_tiles(int epi, int mt, int N) {
+  if (gemm_wide_wgs(epi, mt, N) > 0) return 6;  // three- and two-pair blocks
   // residual projections with 2-7 row tiles: four-tile blocks over a share of
   // K (gemm_ksplit), so each workgroup re-reads a quarter of the activation
   // tiles that a one-tile block over all of K would
