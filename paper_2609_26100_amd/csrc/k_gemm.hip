@@ -678,7 +678,8 @@ __global__ __launch_bounds__(512) void k_gemm(GemmArgs a) {
 // divide into equal blocks that fill it: workgroups [0, wide_wgs) take
 // NT / 2 pairs, the rest NT / 2 - 1 (7B with 2-4 row tiles: 176 x 3 + 80 x 2
 // = 688 pairs, instead of 172 blocks of 4 pairs that leave 84 CUs idle
-// while each busy CU streams 1.5 MiB).
+// while each busy CU streams 1.5 MiB; 13B with 5 row tiles: 96 x 4 + 160 x 3
+// = 864 pairs, instead of 432 blocks of 2 in two rounds).
 template <typename T, int MT, int NT>
 __global__ __launch_bounds__(512) void k_gemm_gu2(GemmArgs a) {
   const int b = blockIdx.x;
@@ -716,6 +717,10 @@ static hipError_t gemm_attr_rows() {
   if constexpr (MT >= 2 && MT <= 4)  // gate/up blocks of three and two pairs
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void*)k_gemm_gu2<T, MT, 6>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)kGemmLdsMax);
+  if constexpr (MT == 5)  // gate/up blocks of four and three pairs
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void*)k_gemm_gu2<T, MT, 8>, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)kGemmLdsMax);
   if constexpr (MT >= 2 && MT <= 4)  // six-tile Q/K/V blocks
     if (e == hipSuccess) e = gemm_attr<T, MT, 6, EPI_QKV>();
@@ -755,16 +760,16 @@ static hipError_t launch_v(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <typename T, int MT>
+template <typename T, int MT, int NT>
 static hipError_t launch_gu2(const GemmArgs& a, hipStream_t s) {
   const int nkc_min = a.nkc;
   int waves = nkc_min < 8 ? nkc_min : 8;
   auto lds_of = [](int w) {
-    const size_t l6 = gemm_lds<MT, 6, EPI_SWIGLU>(w), l4 = gemm_lds<MT, 4, EPI_SWIGLU>(w);
-    return l6 > l4 ? l6 : l4;
+    const size_t lw = gemm_lds<MT, NT, EPI_SWIGLU>(w), ln = gemm_lds<MT, NT - 2, EPI_SWIGLU>(w);
+    return lw > ln ? lw : ln;
   };
-  while (waves > 1 && lds_of(waves) > gemm_lds_cap<MT, 6>()) waves >>= 1;
-  TSS_LAUNCH((k_gemm_gu2<T, MT, 6>), dim3(kGemmRound), dim3(waves * 64), lds_of(waves), s, a);
+  while (waves > 1 && lds_of(waves) > gemm_lds_cap<MT, NT>()) waves >>= 1;
+  TSS_LAUNCH((k_gemm_gu2<T, MT, NT>), dim3(kGemmRound), dim3(waves * 64), lds_of(waves), s, a);
   return hipGetLastError();
 }
 
@@ -789,11 +794,13 @@ static hipError_t launch_rows(int epi, int nt, const GemmArgs& a, hipStream_t s)
     case 3: return epi == EPI_QKV ? launch_v<T, MT, 3, EPI_QKV>(a, s) : hipErrorInvalidValue;
     case 8:
       if constexpr (MT >= 2 && MT <= 4) return epi == EPI_SWIGLU ? launch_v<T, MT, 8, EPI_SWIGLU>(a, s) : hipErrorInvalidValue;
+      if constexpr (MT == 5)
+        if (epi == EPI_SWIGLU && a.wide_wgs > 0) return launch_gu2<T, MT, 8>(a, s);
       return hipErrorInvalidValue;
     case 6:
       if constexpr (MT >= 2 && MT <= 4) {
         if (epi == EPI_QKV) return launch_v<T, MT, 6, EPI_QKV>(a, s);
-        if (epi == EPI_SWIGLU && a.wide_wgs > 0) return launch_gu2<T, MT>(a, s);
+        if (epi == EPI_SWIGLU && a.wide_wgs > 0) return launch_gu2<T, MT, 6>(a, s);
       }
       return hipErrorInvalidValue;
     case 10:

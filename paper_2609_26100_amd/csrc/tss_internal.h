@@ -357,19 +357,27 @@ int verify_in_workspace(tss_ctx* c, uint8_t* base, int32_t seq, const int32_t* t
 // Workgroups of one projection round on this GPU (one per CU).
 constexpr int kGemmRound = 256;
 
-// Gate/up with 2-4 row tiles whose pairs (N / 32) lie between two and three
-// per workgroup of a 256-workgroup round: blocks of three pairs (six tiles)
-// for the first `pairs - 512` workgroups and of two for the rest, so every
-// CU streams (7B: 176 x 3 + 80 x 2 pairs instead of 172 x 4).  Returns that
-// count of three-pair workgroups, or 0.
-inline int gemm_wide_wgs(int epi, int mt, int N) {
-  if (epi != EPI_SWIGLU || mt < 2 || mt > 4 || N % 32) return 0;
+// Gate/up in one round of 256 workgroups of two block widths: with 2-4 row
+// tiles where the pairs (N / 32) lie between two and three per workgroup,
+// three pairs (six tiles) for the first `pairs - 512` workgroups and two for
+// the rest (7B: 176 x 3 + 80 x 2 pairs instead of 172 x 4, which left CUs
+// idle); with 5 row tiles where they lie between three and four, four and
+// three pairs (13B: 96 x 4 + 160 x 3 instead of 432 x 2 in two rounds).
+// Returns that count of wider workgroups, or 0.
+inline int gemm_wide_pairs(int epi, int mt, int N) {
+  if (epi != EPI_SWIGLU || N % 32) return 0;
   const int pairs = N / 32;
-  return pairs > 2 * kGemmRound && pairs <= 3 * kGemmRound ? pairs - 2 * kGemmRound : 0;
+  if (mt >= 2 && mt <= 4 && pairs > 2 * kGemmRound && pairs <= 3 * kGemmRound) return 3;
+  if (mt == 5 && pairs > 3 * kGemmRound && pairs <= 4 * kGemmRound) return 4;
+  return 0;
+}
+inline int gemm_wide_wgs(int epi, int mt, int N) {
+  const int w = gemm_wide_pairs(epi, mt, N);
+  return w ? N / 32 - (w - 1) * kGemmRound : 0;
 }
 
 inline int gemm_tiles(int epi, int mt, int N) {
-  if (gemm_wide_wgs(epi, mt, N) > 0) return 6;  // three- and two-pair blocks
+  if (gemm_wide_pairs(epi, mt, N) > 0) return 2 * gemm_wide_pairs(epi, mt, N);  // blocks of two widths
   // residual projections with 2-7 row tiles: four-tile blocks over a share of
   // K (gemm_ksplit), so each workgroup re-reads a quarter of the activation
   // tiles that a one-tile block over all of K would
