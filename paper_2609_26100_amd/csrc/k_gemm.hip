@@ -714,6 +714,8 @@ static hipError_t gemm_attr_rows() {
   if (e == hipSuccess) e = gemm_attr<T, MT, 3, EPI_QKV>();  // three-tile blocks: Q/K/V only
   if constexpr (MT >= 2 && MT <= 4)  // eight-tile gate/up blocks (four pairs)
     if (e == hipSuccess) e = gemm_attr<T, MT, 8, EPI_SWIGLU>();
+  if constexpr (MT >= 2 && MT <= 4)  // eight-tile lm_head blocks
+    if (e == hipSuccess) e = gemm_attr<T, MT, 8, EPI_LOGITS>();
   if constexpr (MT >= 2 && MT <= 4)  // gate/up blocks of three and two pairs
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void*)k_gemm_gu2<T, MT, 6>, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -793,6 +795,8 @@ static hipError_t launch_rows(int epi, int nt, const GemmArgs& a, hipStream_t s)
     case 4: return launch_mt<T, MT, 4>(epi, a, s);
     case 3: return epi == EPI_QKV ? launch_v<T, MT, 3, EPI_QKV>(a, s) : hipErrorInvalidValue;
     case 8:
+      if constexpr (MT >= 2 && MT <= 4)
+        if (epi == EPI_LOGITS) return launch_v<T, MT, 8, EPI_LOGITS>(a, s);
       if constexpr (MT >= 2 && MT <= 4) return epi == EPI_SWIGLU ? launch_v<T, MT, 8, EPI_SWIGLU>(a, s) : hipErrorInvalidValue;
       if constexpr (MT == 5)
         if (epi == EPI_SWIGLU && a.wide_wgs > 0) return launch_gu2<T, MT, 8>(a, s);

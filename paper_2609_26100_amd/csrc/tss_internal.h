@@ -397,6 +397,10 @@ inline int gemm_tiles(int epi, int mt, int N) {
   if (epi == EPI_QKV && mt >= 2 && mt <= 4 && N % 96 == 0 && N / 96 <= 256 && N / 96 > 192 && N / 64 > 256) return 6;
   if (epi == EPI_SWIGLU) return (mt == 1 || N % 64) ? 2 : 4;
   if (mt == 1 && epi == EPI_LOGITS) return 1;
+  // lm_head with 2-4 row tiles: eight-tile blocks in one round where four-tile
+  // ones need two (32000-token vocabulary: 250 instead of 500 workgroups;
+  // with 5 row tiles they would spill)
+  if (epi == EPI_LOGITS && mt >= 2 && mt <= 4 && N % 128 == 0 && N / 128 <= 256 && N / 64 > 256) return 8;
   // three-tile Q/K/V blocks where they fill one round better than four-tile
   // ones can (more than 192 and at most 256 workgroups: the 7B shape's 256)
   if (epi == EPI_QKV && N % 48 == 0 && N / 48 <= 256 && N / 48 > 192) return 3;
