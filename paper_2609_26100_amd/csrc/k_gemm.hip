@@ -203,6 +203,7 @@ __device__ __forceinline__ void gemm_body(GemmArgs a, int pair0 = 0) {
   __shared__ int s_slot[EPI == EPI_QKV ? kMaxRows : 1];
   __shared__ int s_pos[EPI == EPI_QKV ? kMaxRows : 1];
   __shared__ int s_page[EPI == EPI_QKV ? kMaxRows : 1];                // KV page of the row's slot
+  __shared__ int2 s_col[EPI == EPI_QKV ? COLS : 1];  // per column: section | head << 2, dim | rotary index << 16
   __shared__ const float* s_gain[EPI == EPI_RESID ? kMaxRows : 1];    // next-norm gain of the row's segment
   if constexpr (EPI == EPI_QKV || EPI == EPI_RESID) {
     for (int r = threadIdx.x; r < M; r += blockDim.x) {
@@ -312,6 +313,17 @@ __device__ __forceinline__ void gemm_body(GemmArgs a, int pair0 = 0) {
     for (int r = threadIdx.x; r < M; r += blockDim.x) {
       const int lp = s_slot[r] >> 4;
       if (rows.on(r)) s_page[r] = lp < a.n_arg_pages ? a.pages[lp] : a.page_table[a.pt_off[s_seq[r]] + lp];
+    }
+    // the strip's columns: section (q, k, v), head, the head dimension the
+    // packing put there and its rotary index (divisions once per column)
+    const int d16 = a.d >> 4, hd16 = a.head_dim >> 4;
+    for (int col = threadIdx.x; col < COLS; col += blockDim.x) {
+      const int n = strip * COLS + col;
+      const int tile = n >> 4, c = n & 15;
+      const int sec = tile / d16, ts = tile % d16;
+      const int head = ts / hd16, t = ts % hd16;
+      const int dim = c < 8 ? 8 * t + c : (a.head_dim >> 1) + 8 * t + (c - 8);
+      s_col[col] = make_int2(sec | head << 2, dim | (8 * t + (c & 7)) << 16);
     }
   }
   if constexpr (EPI == EPI_RESID) {
@@ -548,7 +560,6 @@ __device__ __forceinline__ void gemm_body(GemmArgs a, int pair0 = 0) {
   const int n0 = strip * COLS;
   if constexpr (EPI == EPI_QKV) {
     const int HD = a.head_dim, d = a.d;
-    const int d16 = d >> 4, hd16 = HD >> 4;
     // Elements in batches of QB per thread (what the launch gives a thread
     // with 8 waves, at most 8): the batch's rotary coefficients are requested
     // together before any of its stores, so they cost one round trip.
@@ -560,17 +571,14 @@ __device__ __forceinline__ void gemm_body(GemmArgs a, int pair0 = 0) {
       for (int j = 0; j < QB; ++j) {
         const int e = e0 + j * (int)blockDim.x;
         if (e < M * COLS) {
-          const int row = e / COLS, col = e % COLS;
-          const int n = n0 + col;
-          const int tile = n >> 4, c = n & 15;
-          sec[j] = tile / d16;
-          const int ts = tile % d16;
-          head[j] = ts / hd16;
-          const int t = ts % hd16;
-          dim[j] = c < 8 ? 8 * t + c : (HD >> 1) + 8 * t + (c - 8);
+          const int row = e / COLS;
+          const int2 ci = s_col[e % COLS];
+          sec[j] = ci.x & 3;
+          head[j] = ci.x >> 2;
+          dim[j] = ci.y & 0xffff;
           // every column has a rotary index (< hd / 2), so the request is in
           // bounds even where the value goes unused (v)
-          cs[j] = a.rope[(size_t)s_pos[row] * (HD >> 1) + 8 * t + (c & 7)];
+          cs[j] = a.rope[(size_t)s_pos[row] * (HD >> 1) + (ci.y >> 16)];
         }
       }
 #pragma unroll
