@@ -84,9 +84,9 @@ def batch_bytes(shape, seqs):
 # that run makes, so FETCH_SIZE is scaled by 2.0 and WRITE_SIZE by 1.0.  The
 # figures hold for the kernel sources hashed here; any change to them voids
 # the traffic field until the counters are taken again.
-GATEUP_COUNTERS = {"fetch_kib": 88384.6, "write_kib": 129.0, "fetch_scale": 2.0, "write_scale": 1.0,
+GATEUP_COUNTERS = {"fetch_kib": 88389.6, "write_kib": 129.0, "fetch_scale": 2.0, "write_scale": 1.0,
                    "sources": ("paper_2609_26100_amd/csrc/k_gemm.hip", "paper_2609_26100_amd/csrc/tss_internal.h"),
-                   "sha256": "9879bbcb3a0a4e5fb737a4f586b42fa02a9d1f5518c34286fcc4bf82e55e4a16"}
+                   "sha256": "95c7f0be30cafe0b63a00396ab3db03750c9b70ff0cc14528b49c1cddc0d0246"}
 
 
 def gateup_traffic():
