@@ -86,7 +86,7 @@ def batch_bytes(shape, seqs):
 # the traffic field until the counters are taken again.
 GATEUP_COUNTERS = {"fetch_kib": 88389.6, "write_kib": 129.0, "fetch_scale": 2.0, "write_scale": 1.0,
                    "sources": ("paper_2609_26100_amd/csrc/k_gemm.hip", "paper_2609_26100_amd/csrc/tss_internal.h"),
-                   "sha256": "95c7f0be30cafe0b63a00396ab3db03750c9b70ff0cc14528b49c1cddc0d0246"}
+                   "sha256": "9d0d605ea39d5b4eb527dff5d778d2ad81d53505cd5fe559a37fa50d7cd55b38"}
 
 
 def gateup_traffic():

@@ -338,22 +338,6 @@ int verify_in_workspace(tss_ctx* c, uint8_t* base, int32_t seq, const int32_t* t
                         int32_t n_nodes, const uint8_t* mask, uint32_t flags, int32_t* accept_len,
                         int32_t* next_token);
 
-// 16-column tiles per workgroup of a projection launch.  A workgroup streams
-// its tiles over all of K, so every workgroup reads all of the step's
-// activation tiles: a wider block makes each activation tile serve more
-// weight tiles, but leaves fewer workgroups.  Measured on the 7B, 13B and
-// 33B shapes (6 to 72 rows): the best width is the narrowest that fits the
-// matrix in one round of at most 256 workgroups (with more than one row tile
-// a workgroup fills a CU), except that with one row tile gate/up keeps one
-// gate/up pair, lm_head one tile, and Q/K/V takes 4 tiles only if that fits
-// 256 workgroups (else 2), and Q/K/V takes 3 tiles when that gives more than
-// 192 and at most 256 workgroups (7B: 256 instead of 192; the 7B k=5 step
-// 3133 -> 3096 us, the 60-node tree 5903 -> 5792 us); with 2-4 row tiles
-// gate/up takes 8 tiles when they fit 256 workgroups (the 60-node tree
-// 5851 -> 5531 us; with 5 row tiles they spill and the 13B batch slows).
-// The residual projections with 2-8 row tiles take four- (two-) tile blocks
-// over a share of K instead (gemm_ksplit; the partial tiles meet through agent-scope
-// accesses, with no device-scope fence).
 // Workgroups of one projection round on this GPU (one per CU).
 constexpr int kGemmRound = 256;
 
@@ -376,6 +360,23 @@ inline int gemm_wide_wgs(int epi, int mt, int N) {
   return w ? N / 32 - (w - 1) * kGemmRound : 0;
 }
 
+// 16-column tiles per workgroup of a projection launch.  A workgroup streams
+// its tiles over all of K, so every workgroup reads all of the step's
+// activation tiles: a wider block makes each activation tile serve more
+// weight tiles, but leaves fewer workgroups.  Measured on the 7B, 13B and
+// 33B shapes (6 to 72 rows): the best width is the narrowest that fits the
+// matrix in one round of at most 256 workgroups (with more than one row tile
+// a workgroup fills a CU), except that with one row tile gate/up keeps one
+// gate/up pair, lm_head one tile, and Q/K/V takes 4 tiles only if that fits
+// 256 workgroups (else 2), and Q/K/V takes 3 tiles when that gives more than
+// 192 and at most 256 workgroups (7B: 256 instead of 192; the 7B k=5 step
+// 3133 -> 3096 us, the 60-node tree 5903 -> 5792 us); with 2-4 row tiles
+// gate/up takes 8 tiles when they fit 256 workgroups (the 60-node tree
+// 5851 -> 5531 us), or blocks of two widths that fill the round exactly
+// (gemm_wide_pairs), and lm_head 8 tiles where 4 would need two rounds.
+// The residual projections with 2-8 row tiles take four- (two-) tile blocks
+// over a share of K instead (gemm_ksplit; the partial tiles meet through agent-scope
+// accesses, with no device-scope fence).
 inline int gemm_tiles(int epi, int mt, int N) {
   if (gemm_wide_pairs(epi, mt, N) > 0) return 2 * gemm_wide_pairs(epi, mt, N);  // blocks of two widths
   // residual projections with 2-7 row tiles: four-tile blocks over a share of
