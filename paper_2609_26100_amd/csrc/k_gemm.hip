@@ -69,12 +69,13 @@ __device__ __forceinline__ uint4 load_stream(const uint8_t* p) {
 // waves a shallower ring streams faster (7B k=5 step 3168 -> 3138 us); the
 // one-row-tile lm_head likewise (three workgroups per CU: 47.7 -> 46.7 us).  The
 // one-row-tile Q/K/V takes 48 (two slots of its three-tile blocks: 19.3 ->
-// 19.0 us on the 7B shape); budgets of 96-192 slow Q/K/V, O and down (by
-// 0.5-1 us each), 48 slows down (19.0 -> 19.4 us) and 32 the whole step.
-// Measured on the 7B projections.
+// 19.0 us on the 7B shape) and 36 in one-tile blocks (three slots in 76
+// VGPRs, so three workgroups share a CU; 48 would take 84); budgets of 96-192
+// slow Q/K/V, O and down (by 0.5-1 us each), 48 slows down (19.0 -> 19.4 us)
+// and 32 the whole step.  Measured on the 7B projections.
 template <int MT, int NT, int S, int EPI> struct Depth {
   static constexpr int per = NT * 4 + MT * S * 4;
-  static constexpr int budget = MT == 1 ? (EPI == EPI_SWIGLU || EPI == EPI_LOGITS ? 32 : (EPI == EPI_QKV ? 48 : 64)) : (MT * NT >= 20 ? 64 : 128);
+  static constexpr int budget = MT == 1 ? (EPI == EPI_SWIGLU || EPI == EPI_LOGITS ? 32 : (EPI == EPI_QKV ? (NT == 1 ? 36 : 48) : 64)) : (MT * NT >= 20 ? 64 : 128);
   static constexpr int raw = budget / per;
   static constexpr int v = raw < 1 ? 1 : (raw > 8 ? 8 : raw);
 };

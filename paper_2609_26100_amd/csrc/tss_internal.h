@@ -402,6 +402,10 @@ inline int gemm_tiles(int epi, int mt, int N) {
   // ones need two (32000-token vocabulary: 250 instead of 500 workgroups;
   // with 5 row tiles they would spill)
   if (epi == EPI_LOGITS && mt >= 2 && mt <= 4 && N % 128 == 0 && N / 128 <= 256 && N / 64 > 256) return 8;
+  // one row tile: one-tile Q/K/V blocks three to a CU where they fill one
+  // such round (7B: 768 workgroups; the 7B k=5 step -20 us against 256
+  // three-tile blocks, one per CU)
+  if (epi == EPI_QKV && mt == 1 && N % 16 == 0 && N / 16 <= 768 && N / 16 > 512) return 1;
   // three-tile Q/K/V blocks where they fill one round better than four-tile
   // ones can (more than 192 and at most 256 workgroups: the 7B shape's 256)
   if (epi == EPI_QKV && N % 48 == 0 && N / 48 <= 256 && N / 48 > 192) return 3;
