@@ -114,18 +114,27 @@ __device__ __forceinline__ int attn_item_groups(const AttnArgs& a, int n_pages, 
   return max(1, min(cap, min((n_pages + kAttnWaves - 1) / kAttnWaves, n_pages / (TSS_ATTN_PART_DIV * T))));
 }
 
-// LDS: q tiles [TMAX][64][NQ] uint4 | m, l [W][16] | O [W][64][OS]
-template <typename TK, int HD, int TMAX>
+// Dynamic LDS: q tiles [TMAX][64][NQ] uint4 | m, l [W][16] | O [W][64][OS].
+// The paired walk over an fp16 KV cache keeps the same areas in static
+// arrays instead: during the walk the O area holds each wave's LDS page
+// slot, written by global -> LDS loads, and with distinct static arrays the
+// compiler can tell those writes from the walk's other LDS accesses (so
+// reading q does not wait for page loads in flight).
+template <typename TK, int HD, int TMAX, bool PAIR>
 constexpr size_t attn_lds() {
   constexpr int NQ = HD / 4 * (int)sizeof(TK) / 16;
   constexpr int OS = HD / 16 * 4 + 1;
-  return (size_t)(TMAX * 64 * NQ * 4 + kAttnWaves * 16 * 2 + kAttnWaves * 64 * OS) * 4;
+  return PAIR && sizeof(TK) == 2 ? 0 : (size_t)(TMAX * 64 * NQ * 4 + kAttnWaves * 16 * 2 + kAttnWaves * 64 * OS) * 4;
 }
+typedef __attribute__((address_space(1))) const void global_cvoid;
+typedef __attribute__((address_space(3))) void lds_void;
 
 // TK = KV element type (_Float16 or float); TW = weight type of the mode
 // (selects the activation plane format of the output); TMAX = most node
-// tiles of an item in this launch.
-template <typename TK, typename TW, int HD, int TMAX>
+// tiles of an item in this launch; PAIR = the paired page walk (launches
+// over one KV sequence; with several sequences the walk with one page ahead
+// in registers measured faster: 13B batch of 8 9.71 against 10.04 ms).
+template <typename TK, typename TW, int HD, int TMAX, bool PAIR>
 __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   constexpr int DL = HD / 4;                         // dims per lane group in Q K^T
   constexpr int NQ = DL * (int)sizeof(TK) / 16;      // 16-byte K/Q chunks per lane
@@ -141,6 +150,13 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
             grp = lane >> 4;
   const int arg_pages = a.n_arg_pages;
   const int32_t* pt = a.page_table;  // this item's row of the page table, set below
+
+  // With the paired walk all of the kernel's LDS is static (see attn_lds):
+  // q tiles, m and l in s_qml, the merge area [W][64][OS] in s_o, which
+  // holds the waves' page slots during the walk
+  constexpr bool kLdsWalk = PAIR && sizeof(TK) == 2;
+  __shared__ __align__(16) float s_o[kLdsWalk ? W * 64 * OS : 4];
+  __shared__ __align__(16) float s_qml[kLdsWalk ? TMAX * 64 * NQ * 4 + W * 16 * 2 : 4];
 
   const size_t blk_elems = 16 * (size_t)HD;
   auto load_phys = [&](int phys, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
@@ -159,15 +175,33 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   // vector load before the walk, so the walk never waits on a page-table
   // read) or, past the wave's 64th page, from the page table.
   int ids = 0;
+  auto page_phys = [&](int p, int it) {
+    if (p < arg_pages) return a.pages[p];
+    if (it < 64) return __builtin_amdgcn_readlane(ids, it);
+    return __builtin_amdgcn_readfirstlane(__builtin_nontemporal_load(pt + p));
+  };
   auto load_page = [&](int p, int it, uint4 (&kreg)[NQ], uint4 (&vreg)[NV]) {
-    int phys;
-    if (p < arg_pages)
-      phys = a.pages[p];
-    else if (it < 64)
-      phys = __builtin_amdgcn_readlane(ids, it);
-    else
-      phys = __builtin_amdgcn_readfirstlane(__builtin_nontemporal_load(pt + p));
-    load_phys(phys, kreg, vreg);
+    load_phys(page_phys(p, it), kreg, vreg);
+  };
+  // The same page into the wave's LDS slot (global -> LDS, no registers):
+  // 16-byte chunk c of lane l lands at pslot[c * 64 + l], K chunks first,
+  // where the walk reads it back into the registers load_phys would fill.
+  // Every wave's slot lies inside its own row range of the merge area
+  // ((NQ + NV) KiB <= 64 * OS floats).
+  uint4* const pslot = (uint4*)(s_o + (kLdsWalk ? wave * 64 * OS : 0));
+  static_assert(!kLdsWalk || (NQ + NV) * 64 * 16 <= 64 * OS * 4, "page slot inside the wave's merge rows");
+  auto dma_page = [&](int p, int it) {
+    const int phys = page_phys(p, it);
+    const TK* kb = (const TK*)a.kv_pages + (((size_t)a.layer * a.n_pages_pool + phys) * 2 * a.n_heads + head) * blk_elems;
+    const TK* vb = kb + (size_t)a.n_heads * blk_elems;
+    const uint4* kp = (const uint4*)(kb + r16 * HD + grp * DL);
+    const uint4* vp = (const uint4*)(vb + grp * HD * 4 + r16 * NO * 4);
+#pragma unroll
+    for (int c = 0; c < NQ; ++c)
+      __builtin_amdgcn_global_load_lds((global_cvoid*)(kp + c), (lds_void*)(pslot + c * 64), 16, 0, 0);
+#pragma unroll
+    for (int c = 0; c < NV; ++c)
+      __builtin_amdgcn_global_load_lds((global_cvoid*)(vp + c), (lds_void*)(pslot + (NQ + c) * 64), 16, 0, 0);
   };
 
   // The wave's first page is requested before anything else when its id is
@@ -207,7 +241,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   // holds q[node][head*HD + grp*DL + 0..DL).  Waves 0..T-1 build one tile
   // each in LDS (all of a lane's loads issued before the first conversion);
   // every wave re-reads them per page.
-  extern __shared__ float smem[];
+  extern __shared__ float smem_dyn[];
+  float* const smem = kLdsWalk ? s_qml : smem_dyn;
   uint4* sm_q = (uint4*)smem;  // [TMAX][64][NQ]
   if (wave < T) {
     const int ln = wave * 16 + r16;  // local node
@@ -257,105 +292,136 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 
   if (!early && p < n_pages) load_page(p, 0, kcur, vcur);
   float* sm_alpha = smem + TMAX * 64 * NQ * 4 + wave * 16;  // the wave's slots of the merge's m array
-  __syncthreads();  // q tiles ready
-  for (int it = 0; p < n_pages; p += stride, ++it) {
-    uint4 knext[NQ], vnext[NV];
-    if (p + stride < n_pages) load_page(p + stride, it + 1, knext, vnext);
-
-#pragma unroll
-    for (int t = 0; t < TMAX; ++t) {
-      if (t >= T) break;
-      f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
-      asm volatile("" ::: "memory");  // re-read the q tile from LDS each page (keeps it out of registers)
-#pragma unroll
-      for (int c = 0; c < NQ; ++c) {
-        const uint4 qv = sm_q[(t * 64 + lane) * NQ + c];
-        if constexpr (sizeof(TK) == 2) {
-          S = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kcur[c]),
-                                                     __builtin_bit_cast(f16x8, qv), S, 0, 0, 0);
-        } else {
-          S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kcur[c].x), __uint_as_float(qv.x), S, 0, 0, 0);
-          S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kcur[c].y), __uint_as_float(qv.y), S, 0, 0, 0);
-          S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kcur[c].z), __uint_as_float(qv.z), S, 0, 0, 0);
-          S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kcur[c].w), __uint_as_float(qv.w), S, 0, 0, 0);
-        }
-      }
-
-      // S[v] = score of token 4*grp+v of this page against local node 16 t + r16.
-      // Only pages that reach past the context hold draft slots, whose
-      // visibility depends on the node (p is uniform, so is the branch).
-      float s[4];
-      float mloc;
-      if ((p + 1) * kPage <= n_kv) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) s[v] = S[v] * a.scale_log2;
-        mloc = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-      } else {
-        mloc = -INFINITY;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int slot = p * kPage + grp * 4 + v;
-          bool vis;
-          if (slot < n_kv) {
-            vis = true;
+  // Folds page pg (K chunks in kc, V chunks in vc) into every row tile's
+  // online-softmax state.
+  auto walk_page = [&](int pg, const uint4 (&kc)[NQ], const uint4 (&vc)[NV]) {
+  #pragma unroll
+      for (int t = 0; t < TMAX; ++t) {
+        if (t >= T) break;
+        f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
+        asm volatile("" ::: "memory");  // re-read the q tile from LDS each page (keeps it out of registers)
+  #pragma unroll
+        for (int c = 0; c < NQ; ++c) {
+          const uint4 qv = sm_q[(t * 64 + lane) * NQ + c];
+          if constexpr (sizeof(TK) == 2) {
+            S = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kc[c]),
+                                                       __builtin_bit_cast(f16x8, qv), S, 0, 0, 0);
           } else {
-            const unsigned j = (unsigned)(slot - n_kv - base[t]);
-            vis = j < 64u && ((anc[t] >> j) & 1ull);
+            S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].x), __uint_as_float(qv.x), S, 0, 0, 0);
+            S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].y), __uint_as_float(qv.y), S, 0, 0, 0);
+            S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].z), __uint_as_float(qv.z), S, 0, 0, 0);
+            S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].w), __uint_as_float(qv.w), S, 0, 0, 0);
           }
-          s[v] = vis ? S[v] * a.scale_log2 : -INFINITY;
-          mloc = fmaxf(mloc, s[v]);
+        }
+
+        // S[v] = score of token 4*grp+v of this page against local node 16 t + r16.
+        // Only pages that reach past the context hold draft slots, whose
+        // visibility depends on the node (p is uniform, so is the branch).
+        float s[4];
+        float mloc;
+        if ((pg + 1) * kPage <= n_kv) {
+  #pragma unroll
+          for (int v = 0; v < 4; ++v) s[v] = S[v] * a.scale_log2;
+          mloc = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+        } else {
+          mloc = -INFINITY;
+  #pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int slot = pg * kPage + grp * 4 + v;
+            bool vis;
+            if (slot < n_kv) {
+              vis = true;
+            } else {
+              const unsigned j = (unsigned)(slot - n_kv - base[t]);
+              vis = j < 64u && ((anc[t] >> j) & 1ull);
+            }
+            s[v] = vis ? S[v] * a.scale_log2 : -INFINITY;
+            mloc = fmaxf(mloc, s[v]);
+          }
+        }
+        // exponentials with the bare v_exp_f32 (results below 2^-126 flush to
+        // zero, which no probability or weight here needs)
+        const float m_new = fmaxf(m_run[t], max_col4(mloc));
+        const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_new);
+        float pv[4];
+        float lsum = 0.f;
+  #pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          pv[v] = __builtin_amdgcn_exp2f(s[v] - m_new);
+          lsum += pv[v];
+        }
+        l_run[t] = l_run[t] * alpha + sum_col4(lsum);
+        m_run[t] = m_new;
+
+        // O rows are nodes 4*grp+v; their rescale factors (one per node column)
+        // pass through this wave's 16 LDS floats: written by the lanes of
+        // group 0, read back as one 16-byte load (a wave's LDS accesses complete
+        // in order, so no barrier is needed; the merge's m slots are free until
+        // the walk ends).
+        if (grp == 0) sm_alpha[r16] = alpha;
+        __builtin_amdgcn_wave_barrier();
+        const float4 av4 = *(const float4*)(sm_alpha + grp * 4);
+        __builtin_amdgcn_wave_barrier();
+        const float av[4] = {av4.x, av4.y, av4.z, av4.w};
+  #pragma unroll
+        for (int v = 0; v < 4; ++v)
+  #pragma unroll
+          for (int n = 0; n < NO; ++n) O[t][n][v] *= av[v];
+
+        if constexpr (sizeof(TK) == 2) {
+          // A = P[node r16][tokens 4*grp..+3]; B = V[tokens 4*grp..+3][dim NO*r16 + n]
+          const unsigned p01 = pack_f16x2(pv[0], pv[1]), p23 = pack_f16x2(pv[2], pv[3]);
+          const f16x4 A = __builtin_bit_cast(f16x4, uint2{p01, p23});
+          const uint2* v2 = (const uint2*)vc;
+  #pragma unroll
+          for (int n = 0; n < NO; ++n)
+            O[t][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(A, __builtin_bit_cast(f16x4, v2[n]), O[t][n], 0, 0, 0);
+        } else {
+          const float* vf = (const float*)vc;
+  #pragma unroll
+          for (int v = 0; v < 4; ++v)
+  #pragma unroll
+            for (int n = 0; n < NO; ++n)
+              O[t][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[v], vf[n * 4 + v], O[t][n], 0, 0, 0);
         }
       }
-      // exponentials with the bare v_exp_f32 (results below 2^-126 flush to
-      // zero, which no probability or weight here needs)
-      const float m_new = fmaxf(m_run[t], max_col4(mloc));
-      const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_new);
-      float pv[4];
-      float lsum = 0.f;
+  };
+  // The paired walk (PAIR, fp16 cache) takes the pages in pairs and keeps
+  // two in flight within the registers of one: the first page of a pair
+  // arrives in kcur/vcur, the second in the wave's LDS slot (global -> LDS).
+  // Once the slot has been read out, the next pair is requested at once (the
+  // slot's page first, then the registers' page), so both loads overlap.
+  if constexpr (kLdsWalk) {
+    if (p + stride < n_pages) dma_page(p + stride, 1);
+    __syncthreads();  // q tiles ready
+    for (int it = 0; p < n_pages; p += 2 * stride, it += 2) {
+      walk_page(p, kcur, vcur);
+      if (p + stride >= n_pages) break;
+      uint4 ks[NQ], vs[NV];
+      asm volatile("" ::: "memory");  // no slot access moves across this point
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        pv[v] = __builtin_amdgcn_exp2f(s[v] - m_new);
-        lsum += pv[v];
-      }
-      l_run[t] = l_run[t] * alpha + sum_col4(lsum);
-      m_run[t] = m_new;
-
-      // O rows are nodes 4*grp+v; their rescale factors (one per node column)
-      // pass through this wave's 16 LDS floats: written by the lanes of
-      // group 0, read back as one 16-byte load (a wave's LDS accesses complete
-      // in order, so no barrier is needed; the merge's m slots are free until
-      // the walk ends).
-      if (grp == 0) sm_alpha[r16] = alpha;
-      __builtin_amdgcn_wave_barrier();
-      const float4 av4 = *(const float4*)(sm_alpha + grp * 4);
-      __builtin_amdgcn_wave_barrier();
-      const float av[4] = {av4.x, av4.y, av4.z, av4.w};
+      for (int c = 0; c < NQ; ++c) ks[c] = pslot[c * 64 + lane];
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-#pragma unroll
-        for (int n = 0; n < NO; ++n) O[t][n][v] *= av[v];
-
-      if constexpr (sizeof(TK) == 2) {
-        // A = P[node r16][tokens 4*grp..+3]; B = V[tokens 4*grp..+3][dim NO*r16 + n]
-        const unsigned p01 = pack_f16x2(pv[0], pv[1]), p23 = pack_f16x2(pv[2], pv[3]);
-        const f16x4 A = __builtin_bit_cast(f16x4, uint2{p01, p23});
-        const uint2* v2 = (const uint2*)vcur;
-#pragma unroll
-        for (int n = 0; n < NO; ++n)
-          O[t][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(A, __builtin_bit_cast(f16x4, v2[n]), O[t][n], 0, 0, 0);
-      } else {
-        const float* vf = (const float*)vcur;
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-#pragma unroll
-          for (int n = 0; n < NO; ++n)
-            O[t][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[v], vf[n * 4 + v], O[t][n], 0, 0, 0);
-      }
+      for (int c = 0; c < NV; ++c) vs[c] = pslot[(NQ + c) * 64 + lane];
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the slot is read out before it is refilled
+      asm volatile("" ::: "memory");
+      if (p + 3 * stride < n_pages) dma_page(p + 3 * stride, it + 3);
+      asm volatile("" ::: "memory");
+      if (p + 2 * stride < n_pages) load_page(p + 2 * stride, it + 2, kcur, vcur);
+      walk_page(p + stride, ks, vs);
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // no page load still writes the slot
+  } else {
+    __syncthreads();  // q tiles ready
+    for (int it = 0; p < n_pages; p += stride, ++it) {
+      uint4 knext[NQ], vnext[NV];
+      if (p + stride < n_pages) load_page(p + stride, it + 1, knext, vnext);
+      walk_page(p, kcur, vcur);
 #pragma unroll
-    for (int c = 0; c < NQ; ++c) kcur[c] = knext[c];
+      for (int c = 0; c < NQ; ++c) kcur[c] = knext[c];
 #pragma unroll
-    for (int c = 0; c < NV; ++c) vcur[c] = vnext[c];
+      for (int c = 0; c < NV; ++c) vcur[c] = vnext[c];
+    }
   }
 
   // Merge the waves' states tile by tile: O = sum_w f_w O_w / sum_w f_w l_w
@@ -365,7 +431,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   // separates the waves' writes from the combination.
   float* sm_m = smem + TMAX * 64 * NQ * 4;  // [W][16], after the q tiles
   float* sm_l = sm_m + W * 16;              // [W][16]
-  float* sm_o = sm_l + W * 16;              // [W][64][OS]
+  float* sm_o = kLdsWalk ? s_o : sm_l + W * 16;  // [W][64][OS]
   auto row_weights = [&](int row, float (&f)[W]) {
     float mx = -1e30f;
 #pragma unroll
@@ -598,8 +664,13 @@ __global__ __launch_bounds__(kMergeRows * HD / 4) void k_attn_merge(AttnArgs a) 
 
 template <typename TK, typename TW, int HD, int TMAX>
 static hipError_t attn_attr() {
-  return hipFuncSetAttribute((const void*)k_attn<TK, TW, HD, TMAX>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             (int)attn_lds<TK, HD, TMAX>());
+  hipError_t e = hipFuncSetAttribute((const void*)k_attn<TK, TW, HD, TMAX, false>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)attn_lds<TK, HD, TMAX, false>());
+  if constexpr (sizeof(TK) == 2)
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void*)k_attn<TK, TW, HD, TMAX, true>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)attn_lds<TK, HD, TMAX, true>());
+  return e;
 }
 
 template <typename TK, typename TW, int HD>
@@ -622,8 +693,19 @@ hipError_t init_kernel_attributes() {
 
 template <typename TK, typename TW, int HD, int TMAX>
 static hipError_t attn_t(int n_seq, const AttnArgs& a, hipStream_t s) {
-  const size_t lds = attn_lds<TK, HD, TMAX>();
-  TSS_LAUNCH((k_attn<TK, TW, HD, TMAX>), dim3(a.n_heads, n_seq, a.groups), dim3(kAttnWaves * 64), lds, s, a);
+  constexpr size_t lds_one = attn_lds<TK, HD, TMAX, false>();
+  bool launched = false;
+  if constexpr (sizeof(TK) == 2) {
+    if (a.pages_per_wg == 0) {  // one KV sequence: the paired walk
+      constexpr size_t lds_pair = attn_lds<TK, HD, TMAX, true>();
+      TSS_LAUNCH((k_attn<TK, TW, HD, TMAX, true>), dim3(a.n_heads, n_seq, a.groups), dim3(kAttnWaves * 64),
+                 lds_pair, s, a);
+      launched = true;
+    }
+  }
+  if (!launched)
+    TSS_LAUNCH((k_attn<TK, TW, HD, TMAX, false>), dim3(a.n_heads, n_seq, a.groups), dim3(kAttnWaves * 64), lds_one,
+               s, a);
   hipError_t e = hipGetLastError();
   if (e == hipSuccess && a.defer_merge) {
     TSS_LAUNCH((k_attn_merge<TW, HD, TMAX>), dim3(a.n_heads, n_seq, TMAX * 16 / kMergeRows),
