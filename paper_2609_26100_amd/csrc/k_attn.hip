@@ -295,96 +295,96 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   // Folds page pg (K chunks in kc, V chunks in vc) into every row tile's
   // online-softmax state.
   auto walk_page = [&](int pg, const uint4 (&kc)[NQ], const uint4 (&vc)[NV]) {
-  #pragma unroll
-      for (int t = 0; t < TMAX; ++t) {
-        if (t >= T) break;
-        f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
-        asm volatile("" ::: "memory");  // re-read the q tile from LDS each page (keeps it out of registers)
-  #pragma unroll
-        for (int c = 0; c < NQ; ++c) {
-          const uint4 qv = sm_q[(t * 64 + lane) * NQ + c];
-          if constexpr (sizeof(TK) == 2) {
-            S = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kc[c]),
-                                                       __builtin_bit_cast(f16x8, qv), S, 0, 0, 0);
-          } else {
-            S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].x), __uint_as_float(qv.x), S, 0, 0, 0);
-            S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].y), __uint_as_float(qv.y), S, 0, 0, 0);
-            S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].z), __uint_as_float(qv.z), S, 0, 0, 0);
-            S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].w), __uint_as_float(qv.w), S, 0, 0, 0);
-          }
-        }
-
-        // S[v] = score of token 4*grp+v of this page against local node 16 t + r16.
-        // Only pages that reach past the context hold draft slots, whose
-        // visibility depends on the node (p is uniform, so is the branch).
-        float s[4];
-        float mloc;
-        if ((pg + 1) * kPage <= n_kv) {
-  #pragma unroll
-          for (int v = 0; v < 4; ++v) s[v] = S[v] * a.scale_log2;
-          mloc = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-        } else {
-          mloc = -INFINITY;
-  #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int slot = pg * kPage + grp * 4 + v;
-            bool vis;
-            if (slot < n_kv) {
-              vis = true;
-            } else {
-              const unsigned j = (unsigned)(slot - n_kv - base[t]);
-              vis = j < 64u && ((anc[t] >> j) & 1ull);
-            }
-            s[v] = vis ? S[v] * a.scale_log2 : -INFINITY;
-            mloc = fmaxf(mloc, s[v]);
-          }
-        }
-        // exponentials with the bare v_exp_f32 (results below 2^-126 flush to
-        // zero, which no probability or weight here needs)
-        const float m_new = fmaxf(m_run[t], max_col4(mloc));
-        const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_new);
-        float pv[4];
-        float lsum = 0.f;
-  #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          pv[v] = __builtin_amdgcn_exp2f(s[v] - m_new);
-          lsum += pv[v];
-        }
-        l_run[t] = l_run[t] * alpha + sum_col4(lsum);
-        m_run[t] = m_new;
-
-        // O rows are nodes 4*grp+v; their rescale factors (one per node column)
-        // pass through this wave's 16 LDS floats: written by the lanes of
-        // group 0, read back as one 16-byte load (a wave's LDS accesses complete
-        // in order, so no barrier is needed; the merge's m slots are free until
-        // the walk ends).
-        if (grp == 0) sm_alpha[r16] = alpha;
-        __builtin_amdgcn_wave_barrier();
-        const float4 av4 = *(const float4*)(sm_alpha + grp * 4);
-        __builtin_amdgcn_wave_barrier();
-        const float av[4] = {av4.x, av4.y, av4.z, av4.w};
-  #pragma unroll
-        for (int v = 0; v < 4; ++v)
-  #pragma unroll
-          for (int n = 0; n < NO; ++n) O[t][n][v] *= av[v];
-
+#pragma unroll
+    for (int t = 0; t < TMAX; ++t) {
+      if (t >= T) break;
+      f32x4 S = f32x4{0.f, 0.f, 0.f, 0.f};
+      asm volatile("" ::: "memory");  // re-read the q tile from LDS each page (keeps it out of registers)
+#pragma unroll
+      for (int c = 0; c < NQ; ++c) {
+        const uint4 qv = sm_q[(t * 64 + lane) * NQ + c];
         if constexpr (sizeof(TK) == 2) {
-          // A = P[node r16][tokens 4*grp..+3]; B = V[tokens 4*grp..+3][dim NO*r16 + n]
-          const unsigned p01 = pack_f16x2(pv[0], pv[1]), p23 = pack_f16x2(pv[2], pv[3]);
-          const f16x4 A = __builtin_bit_cast(f16x4, uint2{p01, p23});
-          const uint2* v2 = (const uint2*)vc;
-  #pragma unroll
-          for (int n = 0; n < NO; ++n)
-            O[t][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(A, __builtin_bit_cast(f16x4, v2[n]), O[t][n], 0, 0, 0);
+          S = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, kc[c]),
+                                                     __builtin_bit_cast(f16x8, qv), S, 0, 0, 0);
         } else {
-          const float* vf = (const float*)vc;
-  #pragma unroll
-          for (int v = 0; v < 4; ++v)
-  #pragma unroll
-            for (int n = 0; n < NO; ++n)
-              O[t][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[v], vf[n * 4 + v], O[t][n], 0, 0, 0);
+          S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].x), __uint_as_float(qv.x), S, 0, 0, 0);
+          S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].y), __uint_as_float(qv.y), S, 0, 0, 0);
+          S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].z), __uint_as_float(qv.z), S, 0, 0, 0);
+          S = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kc[c].w), __uint_as_float(qv.w), S, 0, 0, 0);
         }
       }
+
+      // S[v] = score of token 4*grp+v of this page against local node 16 t + r16.
+      // Only pages that reach past the context hold draft slots, whose
+      // visibility depends on the node (pg is uniform, so is the branch).
+      float s[4];
+      float mloc;
+      if ((pg + 1) * kPage <= n_kv) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s[v] = S[v] * a.scale_log2;
+        mloc = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+      } else {
+        mloc = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int slot = pg * kPage + grp * 4 + v;
+          bool vis;
+          if (slot < n_kv) {
+            vis = true;
+          } else {
+            const unsigned j = (unsigned)(slot - n_kv - base[t]);
+            vis = j < 64u && ((anc[t] >> j) & 1ull);
+          }
+          s[v] = vis ? S[v] * a.scale_log2 : -INFINITY;
+          mloc = fmaxf(mloc, s[v]);
+        }
+      }
+      // exponentials with the bare v_exp_f32 (results below 2^-126 flush to
+      // zero, which no probability or weight here needs)
+      const float m_new = fmaxf(m_run[t], max_col4(mloc));
+      const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_new);
+      float pv[4];
+      float lsum = 0.f;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        pv[v] = __builtin_amdgcn_exp2f(s[v] - m_new);
+        lsum += pv[v];
+      }
+      l_run[t] = l_run[t] * alpha + sum_col4(lsum);
+      m_run[t] = m_new;
+
+      // O rows are nodes 4*grp+v; their rescale factors (one per node column)
+      // pass through this wave's 16 LDS floats: written by the lanes of
+      // group 0, read back as one 16-byte load (a wave's LDS accesses complete
+      // in order, so no barrier is needed; the merge's m slots are free until
+      // the walk ends).
+      if (grp == 0) sm_alpha[r16] = alpha;
+      __builtin_amdgcn_wave_barrier();
+      const float4 av4 = *(const float4*)(sm_alpha + grp * 4);
+      __builtin_amdgcn_wave_barrier();
+      const float av[4] = {av4.x, av4.y, av4.z, av4.w};
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+#pragma unroll
+        for (int n = 0; n < NO; ++n) O[t][n][v] *= av[v];
+
+      if constexpr (sizeof(TK) == 2) {
+        // A = P[node r16][tokens 4*grp..+3]; B = V[tokens 4*grp..+3][dim NO*r16 + n]
+        const unsigned p01 = pack_f16x2(pv[0], pv[1]), p23 = pack_f16x2(pv[2], pv[3]);
+        const f16x4 A = __builtin_bit_cast(f16x4, uint2{p01, p23});
+        const uint2* v2 = (const uint2*)vc;
+#pragma unroll
+        for (int n = 0; n < NO; ++n)
+          O[t][n] = __builtin_amdgcn_mfma_f32_16x16x16f16(A, __builtin_bit_cast(f16x4, v2[n]), O[t][n], 0, 0, 0);
+      } else {
+        const float* vf = (const float*)vc;
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+          for (int n = 0; n < NO; ++n)
+            O[t][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(pv[v], vf[n * 4 + v], O[t][n], 0, 0, 0);
+      }
+    }
   };
   // The paired walk (PAIR, fp16 cache) takes the pages in pairs and keeps
   // two in flight within the registers of one: the first page of a pair
